@@ -1,0 +1,515 @@
+"""Pins of the fp64 oracle against facts fixed by the paper and by mathematics,
+independent of the oracle's own formulas (CPU only).
+
+Each check is a plain function so that the mutation tests at the bottom can
+plant a plausible mistake in the oracle and confirm that some pin catches it.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.linalg
+import torch
+
+from oracle import mla_oracle as M
+from workloads import make_custom, make_workload
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def rel(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return np.abs(a - b).max() / max(np.abs(b).max(), 1e-300)
+
+
+# ----------------------------------------------------------------------------
+# RoPE: eq:rope, the rotation group, and an independent complex-number form
+# ----------------------------------------------------------------------------
+def complex_rope(x, angle, base):
+    """Half-split RoPE written as complex multiplication: pair j is the complex
+    number x_j + i x_{j+h}, multiplied by exp(i * angle * base^(-2j/d))."""
+    x = np.asarray(x, dtype=np.float64)
+    d = x.shape[-1]
+    h = d // 2
+    z = x[..., :h] + 1j * x[..., h:]
+    th = np.array([base ** (-2.0 * j / d) for j in range(h)])
+    z = z * np.exp(1j * np.asarray(angle, dtype=np.float64)[..., None] * th)
+    return np.concatenate([z.real, z.imag], axis=-1)
+
+
+def check_rope_complex():
+    rng = np.random.default_rng(1)
+    for d in (4, 16, 64):
+        x = rng.standard_normal((7, d))
+        a = rng.integers(-300000, 300000, size=7)
+        assert rel(M.rope(x, a, 10000.0), complex_rope(x, a, 10000.0)) < 1e-9
+
+
+def check_rope_theta_closed_form():
+    # base 10000, d = 16: theta_j = 10^(-j/2); d = 64: theta_j = 10^(-j/8)
+    assert rel(M.rope_theta(16, 10000.0), 10.0 ** (-np.arange(8) / 2.0)) < 1e-14
+    assert rel(M.rope_theta(64, 10000.0), 10.0 ** (-np.arange(32) / 8.0)) < 1e-14
+    # d = 2 is the textbook 2x2 rotation by the angle itself
+    a = 0.7
+    x = np.array([1.3, -0.4])
+    rot = np.array([[math.cos(a), -math.sin(a)], [math.sin(a), math.cos(a)]]) @ x
+    assert rel(M.rope(x, a, 10000.0), rot) < 1e-15
+
+
+def check_rope_relative_identity():
+    """eq:rope: <R(p_q) q, R(p_k + D) k> = <R(p_q - D) q, R(p_k) k>."""
+    rng = np.random.default_rng(2)
+    for d in (16, 64):
+        for _ in range(20):
+            q, k = rng.standard_normal(d), rng.standard_normal(d)
+            pq, pk, dd = rng.integers(0, 270000, size=3)
+            lhs = M.rope(q, pq, 1e4) @ M.rope(k, pk + dd, 1e4)
+            rhs = M.rope(q, pq - dd, 1e4) @ M.rope(k, pk, 1e4)
+            assert abs(lhs - rhs) < 1e-9 * (1 + abs(lhs))
+            ab = M.rope(M.rope(q, pq, 1e4), pk, 1e4)
+            assert rel(ab, M.rope(q, pq + pk, 1e4)) < 1e-9
+            assert abs(np.linalg.norm(M.rope(q, pq, 1e4)) - np.linalg.norm(q)) < 1e-12
+
+
+def test_rope_complex_form():
+    check_rope_complex()
+
+
+def test_rope_theta_closed_form():
+    check_rope_theta_closed_form()
+
+
+def test_rope_relative_identity():
+    check_rope_relative_identity()
+
+
+# ----------------------------------------------------------------------------
+# E1: relocated, segment-wise, merged attention == direct attention
+# ----------------------------------------------------------------------------
+def _family(seed):
+    rng = np.random.default_rng(seed)
+    nd = int(rng.integers(1, 7))
+    lens = [int(x) for x in rng.integers(1, 41, size=nd)]
+    perm = [int(x) for x in rng.permutation(nd)]
+    G = int(rng.integers(1, 4))
+    hpg = int(rng.integers(1, 4))
+    d_c = int(rng.choice([16, 64]))
+    d_r = int(rng.choice([4, 16]))
+    tq = int(rng.integers(0, 9))
+    if sum(lens) + tq == 0:
+        tq = 1
+    return make_custom(lens, req_perm=perm, tq=tq, H=G * hpg, G=G, d_c=d_c, d_r=d_r,
+                       d_model=8 * G, prot_frac=0.3, seed=seed)
+
+
+def check_factorized_equals_direct(wl):
+    g = wl.geom
+    kv = wl.kv(exact=True)
+    q = wl.q_full(exact=True)
+    keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    _, _, pos = M.row_geometry(wl.segs)
+    worst = 0.0
+    for r in range(wl.n_rows):
+        od, ld = M.attend_direct(keys, q[r], int(pos[r]), g.softmax_scale)
+        of, lf = M.attend_factorized(kv, wl.segs, q[r], int(pos[r]), g.softmax_scale,
+                                     g.d_latent, g.rope_base)
+        worst = max(worst, rel(of, od), np.abs(lf - ld).max() / (1 + np.abs(ld).max()))
+    assert worst < 1e-11, worst
+
+
+def test_factorized_equals_direct_tiny_workload():
+    check_factorized_equals_direct(make_workload(1))
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_factorized_equals_direct_random_family(seed):
+    check_factorized_equals_direct(_family(seed))
+
+
+# ----------------------------------------------------------------------------
+# E2: the merge
+# ----------------------------------------------------------------------------
+def check_merge():
+    rng = np.random.default_rng(3)
+    o = rng.standard_normal((6, 5, 32))
+    lse = rng.standard_normal((6, 5)) * 30
+    a, la = M.lse_merge(o, lse)
+    p = rng.permutation(6)
+    b, lb = M.lse_merge(o[p], lse[p])
+    assert rel(a, b) < 1e-13 and rel(la, lb) < 1e-13
+    one, l1 = M.lse_merge(o[:1], lse[:1])
+    assert rel(one, o[0]) < 1e-15 and rel(l1, lse[0]) < 1e-15
+    eq, le = M.lse_merge(o[:2], np.stack([lse[0], lse[0]]))
+    assert rel(eq, 0.5 * (o[0] + o[1])) < 1e-14
+    assert rel(le, lse[0] + math.log(2.0)) < 1e-14
+    # merging the softmax statistics of two halves of a score vector equals the
+    # softmax over the whole vector (brute force)
+    s = rng.standard_normal(50) * 4
+    v = rng.standard_normal((50, 8))
+    w = np.exp(s - s.max())
+    full = (w / w.sum()) @ v
+    lfull = s.max() + math.log(w.sum())
+    parts = []
+    for lo, hi in ((0, 17), (17, 50)):
+        ww = np.exp(s[lo:hi] - s[lo:hi].max())
+        parts.append(((ww / ww.sum()) @ v[lo:hi], s[lo:hi].max() + math.log(ww.sum())))
+    mo, ml = M.lse_merge(np.stack([p_[0] for p_ in parts]), np.array([p_[1] for p_ in parts]))
+    assert rel(mo, full) < 1e-13 and abs(ml - lfull) < 1e-12
+
+
+def test_merge():
+    check_merge()
+
+
+# ----------------------------------------------------------------------------
+# E3: protected everywhere => z = W_o^T O_full (block-diagonal W_o built by scipy)
+# E8: every head Global => no artifact, z = full recompute
+# ----------------------------------------------------------------------------
+def _w_matrix(wl, w_o):
+    """The full first projection as one [H*d_c, d_model] matrix: block-diagonal
+    over projection groups (scipy's block_diag), the plain W_o when n_pg = 1."""
+    return scipy.linalg.block_diag(*[np.asarray(w, dtype=np.float64) for w in w_o])
+
+
+def check_full_projection(wl):
+    g = wl.geom
+    w_o = wl.w_o(exact=True)
+    nan = np.full((wl.n_rows, g.d_model), np.nan)
+    res = M.reference_rows(wl, np.arange(wl.n_rows), z_off=nan, exact=True)
+    o_full, _ = M.full_recompute_rows(wl, np.arange(wl.n_rows), exact=True)
+    z_ref = o_full.reshape(wl.n_rows, -1) @ _w_matrix(wl, w_o)
+    assert np.isfinite(res.z).all()
+    assert rel(res.z, z_ref) < 1e-12
+    # Global + Local contributions equal the full projection
+    _, z_full = M.full_recompute_rows(wl, np.arange(wl.n_rows), exact=True)
+    assert rel(z_full, z_ref) < 1e-12
+
+
+def test_all_protected_is_full_projection_grouped():
+    wl = make_custom([9, 14, 5], req_perm=[2, 0, 1], tq=4, H=6, G=3, d_c=16, d_r=4, d_model=12,
+                     seed=5, prot_rows=np.arange(32))
+    check_full_projection(wl)
+
+
+def test_all_protected_is_full_projection_dense():
+    wl = make_custom([9, 14], req_perm=[1, 0], tq=4, H=4, G=2, d_c=16, d_r=4, d_model=10,
+                     n_pg=1, seed=6, prot_rows=np.arange(27))
+    check_full_projection(wl)
+
+
+def check_all_global(wl):
+    z_off = M.artifact(wl, exact=True)
+    assert np.all(z_off == 0.0)
+    res = M.reference_rows(wl, np.arange(wl.n_rows), z_off=z_off, exact=True)
+    _, z_full = M.full_recompute_rows(wl, np.arange(wl.n_rows), exact=True)
+    assert rel(res.z, z_full) < 1e-12
+
+
+def test_all_global_heads_is_full_recompute():
+    wl = make_custom([12, 7, 9], req_perm=[1, 2, 0], tq=3, H=3, G=3, d_c=16, d_r=4, d_model=9,
+                     seed=7, prot_frac=0.2)
+    check_all_global(wl)
+
+
+# ----------------------------------------------------------------------------
+# E4: the first document of a request is a prefix (offset 0): its artifact is exact
+# ----------------------------------------------------------------------------
+def check_prefix_document(wl):
+    z_off = M.artifact(wl, exact=True)
+    seg0 = wl.segs[np.argmin(wl.segs[:, 2])]
+    assert seg0[2] == 0
+    rows = [r for r in range(seg0[0], seg0[0] + seg0[1]) if r not in set(wl.prot_rows.tolist())]
+    assert rows
+    res = M.reference_rows(wl, rows, z_off=z_off, exact=True)
+    _, z_full = M.full_recompute_rows(wl, rows, exact=True)
+    assert rel(res.z, z_full) < 1e-12
+    # a relocated document's artifact is NOT exact (Local heads see only their document)
+    seg1 = wl.segs[np.argsort(wl.segs[:, 2])[1]]
+    rows1 = [r for r in range(seg1[0], seg1[0] + seg1[1]) if r not in set(wl.prot_rows.tolist())]
+    res1 = M.reference_rows(wl, rows1, z_off=z_off, exact=True)
+    _, z_full1 = M.full_recompute_rows(wl, rows1, exact=True)
+    assert rel(res1.z, z_full1) > 1e-6
+
+
+def test_prefix_document_artifact_is_exact():
+    wl = make_custom([10, 13, 8], req_perm=[1, 0, 2], tq=4, H=4, G=2, d_c=16, d_r=4, d_model=8,
+                     seed=8, prot_frac=0.25)
+    check_prefix_document(wl)
+
+
+def test_tiny_workload_prefix_document():
+    check_prefix_document(make_workload(1))
+
+
+# ----------------------------------------------------------------------------
+# E5: protected rows replace the artifact (never read, never added)
+# ----------------------------------------------------------------------------
+def test_protected_rows_never_read_artifact():
+    wl = make_workload(1)
+    z_off = M.artifact(wl, exact=True)
+    rows = np.arange(wl.n_rows)
+    a = M.reference_rows(wl, rows, z_off=z_off, exact=True)
+    poisoned = z_off.copy()
+    poisoned[wl.prot_rows] = np.nan
+    b = M.reference_rows(wl, rows, z_off=poisoned, exact=True)
+    assert np.isfinite(b.z).all()
+    assert np.array_equal(a.z, b.z)
+    # unprotected rows do add it
+    un = np.setdiff1d(rows, wl.prot_rows)
+    assert rel(a.z[un] - a.z_online[un], z_off[un]) < 1e-15
+
+
+# ----------------------------------------------------------------------------
+# E7: closed forms of softmax attention
+# ----------------------------------------------------------------------------
+def test_closed_forms():
+    wl = make_custom([6, 9], req_perm=[1, 0], tq=3, H=2, G=1, d_c=16, d_r=4, d_model=4, seed=9)
+    g = wl.geom
+    kv = wl.kv(exact=True).astype(np.float64)
+    keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    _, _, pos = M.row_geometry(wl.segs)
+    order = np.argsort(pos)
+    for r in range(wl.n_rows):
+        t = int(pos[r])
+        o, lse = M.attend_direct(keys, np.zeros((1, g.d_qk)), t, g.softmax_scale)
+        vis = kv[order[: t + 1], : g.d_latent]
+        assert rel(o[0], vis.mean(axis=0)) < 1e-13
+        assert abs(lse[0] - math.log(t + 1)) < 1e-13
+    # the row at request position 0 sees exactly one key: itself
+    r0 = int(order[0])
+    q = wl.q_full(exact=True)[r0]
+    o, lse = M.attend_direct(keys, q, 0, g.softmax_scale)
+    assert rel(o, np.broadcast_to(kv[r0, : g.d_latent], o.shape)) < 1e-15
+    s = g.softmax_scale * (q[:, : g.d_latent] @ kv[r0, : g.d_latent]
+                           + M.rope(q[:, g.d_latent:], 0, g.rope_base) @ kv[r0, g.d_latent:])
+    assert rel(lse, s) < 1e-13
+
+
+# ----------------------------------------------------------------------------
+# E9: one document at offset 0 with every row protected is textbook causal
+# attention: compare with torch's scaled_dot_product_attention (fp64, CPU)
+# ----------------------------------------------------------------------------
+def check_textbook_sdpa():
+    wl = make_custom([37], tq=0, H=3, G=1, d_c=64, d_r=16, d_model=8, seed=10,
+                     prot_rows=np.arange(37))
+    g = wl.geom
+    kv = wl.kv(exact=True)
+    q = wl.q_full(exact=True)                           # [T, H, D]
+    t = np.arange(wl.n_rows)
+    # true-position queries via the complex form; canonical keys at offset 0 are true keys
+    qt = np.concatenate([q[..., : g.d_latent],
+                         complex_rope(q[..., g.d_latent:], np.repeat(t[:, None], g.n_heads, 1), 1e4)], -1)
+    Q = torch.from_numpy(qt.transpose(1, 0, 2).copy())              # [H, T, D]
+    K = torch.from_numpy(kv.astype(np.float64))[None].expand(g.n_heads, -1, -1)
+    V = torch.from_numpy(kv[:, : g.d_latent].astype(np.float64))[None].expand(g.n_heads, -1, -1)
+    ref = torch.nn.functional.scaled_dot_product_attention(Q, K, V, is_causal=True,
+                                                           scale=g.softmax_scale).numpy()
+    keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    for r in range(wl.n_rows):
+        o, _ = M.attend_direct(keys, q[r], r, g.softmax_scale)
+        assert rel(o, ref[:, r, :]) < 1e-12
+
+
+def test_textbook_sdpa():
+    check_textbook_sdpa()
+
+
+# ----------------------------------------------------------------------------
+# needles: a planted key dominates exactly the rows that can see it
+# ----------------------------------------------------------------------------
+def test_needle_visibility():
+    wl = make_custom([20, 16, 24], req_perm=[2, 0, 1], tq=6, H=2, G=1, d_c=16, d_r=16, d_model=4,
+                     seed=11)
+    g = wl.geom
+    kv = wl.kv(exact=True).astype(np.float64)
+    q = wl.q_full(exact=True)
+    seg, u, pos = M.row_geometry(wl.segs)
+    r = wl.n_rows - 1                       # last query row
+    t = int(pos[r])
+    s = int(np.argsort(wl.segs[:, 2])[1])   # second document in request order
+    ks, ln, ps = wl.segs[s]
+    j = int(ks + 5)
+    qr = q[r, 0, g.d_latent:]
+    # canonical-frame key aligned with the relocated query: score ~ +40
+    kv[j, g.d_latent:] = 40.0 / g.softmax_scale * M.rope(qr, t - ps, g.rope_base) / (qr @ qr)
+    kv[j, : g.d_latent] = 0.0
+    kv[j, 0] = 5.0
+    keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    o, lse = M.attend_direct(keys, q[r], t, g.softmax_scale)
+    assert abs(o[0, 0] - 5.0) < 1e-6 and np.abs(o[0, 1:]).max() < 1e-6
+    of, _ = M.attend_factorized(kv, wl.segs, q[r], t, g.softmax_scale, g.d_latent, g.rope_base)
+    assert rel(of, o) < 1e-11
+    # a row placed just before the needle cannot see it
+    rb = int(np.nonzero(pos == pos[j] - 1)[0][0])
+    kv2 = kv.copy()
+    kv2[j] = wl.kv(exact=True)[j]
+    a, _ = M.attend_direct(keys, q[rb], int(pos[rb]), g.softmax_scale)
+    b, _ = M.attend_direct(M.TrueKeys(kv2, wl.segs, g.d_latent, g.rope_base), q[rb], int(pos[rb]),
+                           g.softmax_scale)
+    assert np.array_equal(a, b)
+
+
+# ----------------------------------------------------------------------------
+# bookkeeping: brute-force visibility and the chunk rule
+# ----------------------------------------------------------------------------
+def check_bookkeeping(wl, split_keys):
+    G, hpg = wl.geom.n_groups, wl.geom.heads_per_group
+    row_src, ptr, pseg = M.enumerate_plan(wl.segs, G, hpg, wl.prot_rows, split_keys)
+    seg, _, pos = M.row_geometry(wl.segs)
+    n = wl.n_rows
+    hl = hpg - 1
+    n_slots = n * G + wl.n_prot * G * hl
+    assert ptr.shape == (n_slots + 1,) and ptr[0] == 0 and np.all(np.diff(ptr) >= 1)
+    assert pseg.shape == (ptr[-1], 2)
+    assert np.array_equal(np.nonzero(row_src)[0], np.asarray(wl.prot_rows))
+    req_rank = np.argsort(np.argsort(wl.segs[:, 2]))
+    # brute force: segment s is visible to row r iff some key of s sits at a
+    # true position <= pos[r]
+    vis = {}
+    for r in range(n):
+        vis[r] = sorted({int(seg[j]) for j in range(n) if pos[j] <= pos[r]}, key=lambda s: req_rank[s])
+
+    def slot_row(i):
+        return i // G if i < n * G else int(wl.prot_rows[(i - n * G) // (G * hl)])
+
+    for i in range(n_slots):
+        parts = pseg[ptr[i]:ptr[i + 1]]
+        covered = []
+        for a, b in parts:
+            ra, rb = req_rank[a], req_rank[b]
+            assert ra <= rb
+            block = [int(s) for s in np.argsort(wl.segs[:, 2])[ra:rb + 1]]
+            if split_keys > 0 and len(block) > 1:
+                assert wl.segs[block, 1].sum() <= split_keys
+            covered += block
+        assert covered == vis[slot_row(i)]
+        if split_keys == 0:
+            assert all(a == b for a, b in parts)
+        elif len(parts) > 1:
+            # greedy: each chunk could not take the next chunk's first segment
+            for (a, b), (c, _) in zip(parts[:-1], parts[1:]):
+                blk = np.argsort(wl.segs[:, 2])[req_rank[a]:req_rank[b] + 1]
+                assert wl.segs[blk, 1].sum() + wl.segs[c, 1] > split_keys
+
+
+@pytest.mark.parametrize("split_keys", [0, 1, 25, 60, 10 ** 9])
+def test_bookkeeping_brute_force(split_keys):
+    wl = make_custom([7, 19, 3, 11], req_perm=[2, 0, 3, 1], tq=5, H=6, G=2, d_c=16, d_r=4,
+                     d_model=8, seed=12, prot_frac=0.3)
+    check_bookkeeping(wl, split_keys)
+
+
+def test_bookkeeping_tiny_workload():
+    check_bookkeeping(make_workload(1), 0)
+
+
+def test_per_segment_partial_counts_large():
+    """Per-segment mode at the 32K shape: a row of the k-th document in request
+    order has exactly k+1 partials per slot (closed form)."""
+    wl = make_workload(3)
+    G, hpg = wl.geom.n_groups, wl.geom.heads_per_group
+    row_src, ptr, pseg = M.enumerate_plan(wl.segs, G, hpg, wl.prot_rows, 0)
+    seg, _, _ = M.row_geometry(wl.segs)
+    rank = np.argsort(np.argsort(wl.segs[:, 2]))
+    cnt = np.diff(ptr)
+    n = wl.n_rows
+    assert np.array_equal(cnt[: n * G], np.repeat(rank[seg] + 1, G))
+    assert np.array_equal(cnt[n * G:], np.repeat(rank[seg[wl.prot_rows]] + 1, G * (hpg - 1)))
+
+
+# ----------------------------------------------------------------------------
+# head partition: the paper's printed structural ceilings (eq:ceiling)
+# ----------------------------------------------------------------------------
+def test_head_partition_printed_ceiling():
+    gold = json.load(open(os.path.join(HERE, "golden", "paper_profiles.json")))["profiles"]
+    for name, p in gold.items():
+        H = p["local_heads"] + p["global_heads"]
+        wl = make_custom([4], tq=0, H=H, G=H // p["heads_per_group"], d_c=16, d_r=4, d_model=8)
+        n_local = wl.local_head_ids().size
+        assert n_local == p["local_heads"]
+        assert len(set(wl.local_head_ids().ravel()) | set(wl.global_head_ids())) == H
+        n_layers = p["fence_front"] + p["reusable"] + p["fence_back"]
+        ceiling = p["reusable"] / n_layers * n_local / H
+        assert round(100 * ceiling, 2) == p["printed_ceiling_percent"], (name, ceiling)
+
+
+# ----------------------------------------------------------------------------
+# mutation tests: a plausible mistake planted in the oracle fails a pin
+# ----------------------------------------------------------------------------
+def _rope_wrong_sign(x, angle, base):
+    return _ORIG["rope"](x, -np.asarray(angle), base)
+
+
+def _rope_wrong_pairs(x, angle, base):
+    x = np.asarray(x, dtype=np.float64)
+    d = x.shape[-1]
+    # adjacent pairs (x_0, x_1), (x_2, x_3), ... instead of half-split pairs
+    perm = np.concatenate([np.arange(0, d, 2), np.arange(1, d, 2)])
+    inv = np.argsort(perm)
+    return _ORIG["rope"](x[..., perm], angle, base)[..., inv]
+
+
+def _theta_off_by_one(d_r, base):
+    j = np.arange(1, d_r // 2 + 1, dtype=np.float64)
+    return np.power(base, -2.0 * j / d_r)
+
+
+def _merge_no_weights(o, lse):
+    o = np.asarray(o, dtype=np.float64)
+    return o.mean(axis=0), np.asarray(lse).max(axis=0)
+
+
+def _blocks_wrong_offset(w_o, n_heads, d_latent, d_model):
+    out = _ORIG["dense_blocks"](w_o, n_heads, d_latent, d_model)
+    return np.roll(out, 1, axis=0) if w_o.shape[0] > 1 else out.transpose(0, 1, 2)[::-1]
+
+
+def _rope_identity(x, angle, base):
+    return np.asarray(x, dtype=np.float64).copy()
+
+
+_ORIG = {k: getattr(M, k) for k in ("rope", "rope_theta", "lse_merge", "dense_blocks", "row_geometry",
+                                    "softmax_stats")}
+
+
+def _softmax_no_max_shift_wrong_lse(scores, values):
+    o, lse = _ORIG["softmax_stats"](scores, values)
+    return o, lse - scores.max(axis=-1)
+
+
+MUTATIONS = {
+    "rope_sign": ("rope", _rope_wrong_sign),
+    "rope_pairs": ("rope", _rope_wrong_pairs),
+    "rope_dropped": ("rope", _rope_identity),
+    "theta_index": ("rope_theta", _theta_off_by_one),
+    "merge_weights": ("lse_merge", _merge_no_weights),
+    "oproj_blocks": ("dense_blocks", _blocks_wrong_offset),
+    "lse_term": ("softmax_stats", _softmax_no_max_shift_wrong_lse),
+}
+
+
+def _all_checks():
+    check_rope_complex()
+    check_rope_theta_closed_form()
+    check_rope_relative_identity()
+    check_merge()
+    check_textbook_sdpa()
+    check_full_projection(make_custom([9, 14, 5], req_perm=[2, 0, 1], tq=4, H=6, G=3, d_c=16, d_r=4,
+                                      d_model=12, seed=5, prot_rows=np.arange(32)))
+    check_factorized_equals_direct(_family(3))
+    test_closed_forms()
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_planted_mistake_is_caught(name, monkeypatch):
+    attr, bad = MUTATIONS[name]
+    monkeypatch.setattr(M, attr, bad)
+    with pytest.raises(AssertionError):
+        _all_checks()
+
+
+def test_unmutated_checks_pass():
+    _all_checks()
