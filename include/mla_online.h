@@ -1,0 +1,209 @@
+/*
+ * mla_online.h -- C ABI of the MLA-Online step of RedKnot-MLA (arXiv 2609.07008)
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The step recomputes, at serving time, the part of a multi-head-latent-attention
+ * layer that cannot be reused from per-document offline artifacts (Sec. 2.3,
+ * Alg. 2):
+ *   1. query-side RoPE relocation: each query is rotated into a document's
+ *      canonical frame, R(t - p_s), instead of rewriting cached keys (eq:rope);
+ *   2. absorbed-MLA attention over the single packed latent stream (d_c latent
+ *      plus d_r decoupled RoPE key per token), one document segment (or one run
+ *      of segments) at a time: Global heads on every row, Local heads only on
+ *      protected rows (SelectiveMLA);
+ *   3. a stable segmented log-sum-exp merge of the per-segment partials;
+ *   4. the group-aligned sliced first output projection W_a, with the offline
+ *      Local-head artifact z_off added on unprotected rows and replaced (never
+ *      added) on protected rows (RestoreAndReplace, eq:factorization).
+ * The shared second projection W_b is outside this library.
+ *
+ * Conventions (all entry points):
+ *  - Host arrays are read during the call only.  Device arrays are owned by the
+ *    caller; the library allocates no device memory (scratch comes in as a
+ *    caller-provided workspace) and keeps no per-call state.
+ *  - All device work is enqueued on `stream` (a hipStream_t passed as void*;
+ *    NULL is the default stream) in call order; nothing is synchronized.  The
+ *    attend call copies a small plan (segment tables and the work list) from a
+ *    library-owned pinned host buffer into the workspace on the same stream.
+ *  - Every entry point validates its arguments on the host before enqueueing
+ *    anything and returns a status; it never aborts and never falls back to a
+ *    different computation.  mla_last_error_detail() describes the last failure
+ *    of the calling thread.
+ *  - Layouts are dense row-major.  "bf16" is IEEE bfloat16 (uint16 storage).
+ *    Device pointers to bf16 or float data must be 16-byte aligned.
+ *  - Supported (d_latent, d_rope): (512, 64) -- the DeepSeek latent row of the
+ *    paper's profiles -- and (64, 16).  Others return MLA_ERR_UNSUPPORTED.
+ *
+ * Notation: N request rows; a row r is also KV row r (storage order); H heads in
+ * G output groups of hpg = H/G heads with one Global head per group (Sec. 3.1);
+ * L_h = G*(hpg-1) Local heads per protected row; P protected rows; D = d_c+d_r.
+ */
+#ifndef MLA_ONLINE_H
+#define MLA_ONLINE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum mla_status {
+  MLA_OK = 0,
+  MLA_ERR_NULL = 1,         /* a required pointer is NULL                           */
+  MLA_ERR_SHAPE = 2,        /* inconsistent sizes, alignment or geometry            */
+  MLA_ERR_UNSUPPORTED = 3,  /* valid but not built (head dims, group counts)        */
+  MLA_ERR_SEGMENTS = 4,     /* segment table does not tile the rows                 */
+  MLA_ERR_ROWS = 5,         /* protected rows unsorted, duplicated or out of range  */
+  MLA_ERR_WORKSPACE = 6,    /* workspace smaller than mla_online_attend_query says  */
+  MLA_ERR_HIP = 7           /* a HIP runtime call or kernel launch failed           */
+} mla_status;
+
+typedef enum mla_dtype { MLA_BF16 = 0, MLA_F32 = 1 } mla_dtype;
+
+/* Layer geometry (Sec. 2.1, Sec. 3.1).
+ *  n_heads        H logical query heads
+ *  n_groups       G native output groups; each holds one Global head
+ *  d_latent       d_c, width of the latent (and of every head's value/output)
+ *  d_rope         d_r, width of the decoupled RoPE key/query part
+ *  d_model        width of the projected state z
+ *  n_proj_groups  n_pg: the first projection W_a is block-diagonal over n_pg
+ *                 projection groups (n_pg = 1 is a dense W_a); n_pg divides G and
+ *                 d_model, and d_model/n_pg is a multiple of 32
+ *  softmax_scale  factor applied to q.k before the softmax (> 0)
+ *  rope_base      RoPE base; frequency j is base^(-2j/d_r), pairs are
+ *                 (x_j, x_{j+d_r/2})                                           */
+typedef struct mla_geom {
+  int32_t n_heads;
+  int32_t n_groups;
+  int32_t d_latent;
+  int32_t d_rope;
+  int32_t d_model;
+  int32_t n_proj_groups;
+  float softmax_scale;
+  double rope_base;
+} mla_geom;
+
+/* One document (or the request-query block) of the request (Sec. 2.3; the
+ * compact segment-pointer geometry of Sec. 3.2).
+ *  kv_start    first storage row of the segment in kv / q_glob / z_off
+ *  length      rows in the segment (>= 1)
+ *  req_offset  request position of the segment's first row (Delta_i); the
+ *              segment's keys are stored in its canonical frame (RoPE at 0..)
+ * Across all segments, [kv_start, kv_start+length) tile [0, N) and so do
+ * [req_offset, req_offset+length).  Storage row kv_start+u sits at request
+ * position req_offset+u.  Segments are identified by their index in the array. */
+typedef struct mla_segment {
+  int64_t kv_start;
+  int64_t length;
+  int64_t req_offset;
+} mla_segment;
+
+/*
+ * Output slots and partials.
+ *   Global slot (r, g)    = r*G + g,                  r in [0,N), g in [0,G)
+ *   Local slot (a, g, j)  = N*G + (a*G + g)*(hpg-1) + j, for protected row
+ *                           prot_rows[a] and the j-th Local head of group g
+ *                           (ascending head index, the Global head skipped)
+ *   n_slots = N*G + P*G*(hpg-1)
+ * A row at request position t sees every segment with req_offset <= t (its own
+ * segment causally, keys u <= t - req_offset), in request order.  That list is
+ * cut into chunks by `split_keys`:
+ *   split_keys == 0  one chunk per visible segment (the per-segment partials of
+ *                    SelectiveMLA in Alg. 2);
+ *   split_keys  > 0  greedy runs of whole segments in request order; a run is
+ *                    closed before a segment that would push its summed segment
+ *                    lengths past split_keys (a run holds at least one segment).
+ *                    A value >= N gives one chunk per slot: the merge is then
+ *                    done entirely inside the attention kernel.
+ * Each slot owns one partial per chunk, stored contiguously in request order;
+ * part_ptr is the CSR offset array over slots.
+ */
+
+/* Size query (host only, pure).  Arguments as for mla_online_attend.  Returns
+ * n_slots, n_parts and the workspace bytes mla_online_attend needs. */
+mla_status mla_online_attend_query(const mla_geom* geom, const mla_segment* segs, int32_t n_segs,
+                                   const int32_t* prot_rows, int32_t n_prot, int64_t split_keys,
+                                   int64_t* n_slots, int64_t* n_parts, size_t* ws_bytes);
+
+/* Steps 1-2: relocation and segment-wise absorbed-MLA attention (Alg. 2,
+ * SelectiveMLA with R(-Delta_i) applied to the query; RestorePhase is the
+ * identity because the value is the latent and carries no rotary part).
+ *  geom, segs, n_segs     host; see above
+ *  prot_rows, n_prot      host int32 [P], strictly increasing storage rows (the
+ *                         protected set A of eq:protected; query rows are
+ *                         normally included)
+ *  split_keys             >= 0, see above
+ *  kv        device bf16 [N, D]: per storage row the latent c (d_c) followed by
+ *            the RoPE key in its segment's canonical frame (d_r)
+ *  q_glob    device bf16 [N, G, D]: absorbed query of each group's Global head,
+ *            RoPE part not yet rotated (it is rotated to the row's position
+ *            relative to each segment inside the kernel)
+ *  q_loc     device bf16 [P, G, hpg-1, D]: Local-head queries of protected rows
+ *            (may be NULL when P == 0 or hpg == 1)
+ *  part_o    device f32 [n_parts, d_c]: normalized partial outputs sum p_j c_j / sum p_j
+ *  part_lse  device f32 [n_parts]: natural-log log-sum-exp of the scaled scores
+ *  part_ptr  device i64 [n_slots + 1]: CSR offsets of each slot's partials
+ *  part_seg  device i32 [n_parts, 2] or NULL: first and last segment index
+ *            covered by each partial
+ *  row_src   device u8 [N] or NULL: 1 where the row is protected (recomputed),
+ *            0 where its Local contribution comes from the artifact
+ *  workspace device scratch of at least the queried size, 256-byte aligned
+ * Errors: NULL, SHAPE, UNSUPPORTED, SEGMENTS, ROWS, WORKSPACE, HIP. */
+mla_status mla_online_attend(const mla_geom* geom, const mla_segment* segs, int32_t n_segs,
+                             const int32_t* prot_rows, int32_t n_prot, int64_t split_keys,
+                             const void* kv, const void* q_glob, const void* q_loc, float* part_o,
+                             float* part_lse, int64_t* part_ptr, int32_t* part_seg, uint8_t* row_src,
+                             void* workspace, size_t ws_bytes, void* stream);
+
+/* Step 3: SegmentedLSEMerge (Alg. 2).  For each slot with partials (o_i, l_i):
+ * m = max l_i, w_i = exp(l_i - m), O = sum w_i o_i / sum w_i,
+ * lse = m + ln sum w_i; a slot with one partial is copied.
+ *  n_slots    number of slots (>= 0)
+ *  d_latent   64 or 512
+ *  part_o, part_lse, part_ptr   device, as written by mla_online_attend
+ *                               (part_ptr[0] must be 0, every slot >= 1 partial)
+ *  out_dtype  MLA_BF16 or MLA_F32: element type of out_o
+ *  out_o      device [n_slots, d_c]; its first N*G rows are O_glob [N, G, d_c]
+ *             and the rest O_loc [P, G, hpg-1, d_c]
+ *  out_lse    device f32 [n_slots] or NULL
+ * Errors: NULL, SHAPE, UNSUPPORTED, HIP. */
+mla_status mla_segment_merge(int64_t n_slots, int32_t d_latent, const float* part_o,
+                             const float* part_lse, const int64_t* part_ptr, int32_t out_dtype,
+                             void* out_o, float* out_lse, void* stream);
+
+/* Step 4: z = W_{a,G} O_G + W_{a,L} O_{L,A} on protected rows, plus z_off on the
+ * other rows (eq:offonline, eq:factorization; RestoreAndReplace of Alg. 2).
+ * Head h of projection group pg = h / (H/n_pg) uses rows
+ * [(h mod H/n_pg)*d_c, +d_c) of w_o[pg] and writes channels
+ * [pg*d_model/n_pg, (pg+1)*d_model/n_pg).
+ *  geom        host
+ *  n_rows      N
+ *  o_glob      device bf16 [N, G, d_c]
+ *  o_loc       device bf16 [P, G, hpg-1, d_c] (NULL allowed when P == 0 or hpg == 1)
+ *  glob_head   host int32 [G]: in-group index (0..hpg-1) of each group's Global head
+ *  prot_rows   device int32 [P]: the same strictly increasing protected rows
+ *  w_o         device bf16 [n_pg, (H/n_pg)*d_c, d_model/n_pg]
+ *  z_off       device bf16 [N, d_model]: projected Local-head artifact; rows in
+ *              the protected set are never read (NULL allowed when P == N)
+ *  z           device f32 [N, d_model], written
+ * Errors: NULL, SHAPE, UNSUPPORTED, ROWS, HIP. */
+mla_status mla_sliced_oproj_add(const mla_geom* geom, int64_t n_rows, const void* o_glob,
+                                const void* o_loc, const int32_t* glob_head,
+                                const int32_t* prot_rows, int32_t n_prot, const void* w_o,
+                                const void* z_off, float* z, void* stream);
+
+/* Static description of a status code. */
+const char* mla_status_str(mla_status s);
+
+/* Detail of the calling thread's last failed call ("" if none). */
+const char* mla_last_error_detail(void);
+
+/* Library version string. */
+const char* mla_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MLA_ONLINE_H */

@@ -1,0 +1,472 @@
+// Host side of the MLA-Online C ABI: argument validation, the plan (segment
+// visibility in request order, chunking of each row's visible-segment list,
+// the partial index and the longest-first work list), and kernel dispatch.
+#include <algorithm>
+#include <cstdarg>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+namespace {
+
+thread_local std::string g_detail;
+
+mla_status fail(mla_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+mla_status fail(mla_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_detail = buf;
+  return s;
+}
+
+mla_status hip_fail(hipError_t e, const char* what) {
+  return fail(MLA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// ---------------------------------------------------------------------------
+// validation
+// ---------------------------------------------------------------------------
+mla_status check_geom(const mla_geom* g, bool for_oproj) {
+  if (g == nullptr) return fail(MLA_ERR_NULL, "geom is NULL");
+  if (g->n_heads < 1 || g->n_groups < 1 || g->n_heads % g->n_groups != 0)
+    return fail(MLA_ERR_SHAPE, "n_heads (%d) must be a positive multiple of n_groups (%d)", g->n_heads,
+                g->n_groups);
+  if (g->n_groups > mla::kMaxGroups)
+    return fail(MLA_ERR_UNSUPPORTED, "n_groups %d exceeds %d", g->n_groups, mla::kMaxGroups);
+  if (!((g->d_latent == 512 && g->d_rope == 64) || (g->d_latent == 64 && g->d_rope == 16)))
+    return fail(MLA_ERR_UNSUPPORTED, "(d_latent, d_rope) = (%d, %d); built: (512, 64), (64, 16)", g->d_latent,
+                g->d_rope);
+  if (!(g->softmax_scale > 0.f) || !std::isfinite(g->softmax_scale))
+    return fail(MLA_ERR_SHAPE, "softmax_scale must be finite and > 0");
+  if (!(g->rope_base > 1.0) || !std::isfinite(g->rope_base))
+    return fail(MLA_ERR_SHAPE, "rope_base must be finite and > 1");
+  if (for_oproj) {
+    if (g->d_model < 1 || g->n_proj_groups < 1 || g->n_groups % g->n_proj_groups != 0 ||
+        g->d_model % g->n_proj_groups != 0)
+      return fail(MLA_ERR_SHAPE, "n_proj_groups (%d) must divide n_groups (%d) and d_model (%d)",
+                  g->n_proj_groups, g->n_groups, g->d_model);
+    if ((g->d_model / g->n_proj_groups) % 32 != 0)
+      return fail(MLA_ERR_UNSUPPORTED, "d_model / n_proj_groups = %d is not a multiple of 32",
+                  g->d_model / g->n_proj_groups);
+  }
+  return MLA_OK;
+}
+
+// Segments: lengths >= 1; storage and request intervals both tile [0, N).
+mla_status check_segments(const mla_segment* segs, int32_t n, int64_t* n_rows) {
+  if (segs == nullptr) return fail(MLA_ERR_NULL, "segs is NULL");
+  if (n < 1) return fail(MLA_ERR_SEGMENTS, "n_segs = %d, need at least one segment", n);
+  int64_t total = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (segs[i].length < 1) return fail(MLA_ERR_SEGMENTS, "segment %d has length %lld", i, (long long)segs[i].length);
+    if (segs[i].kv_start < 0 || segs[i].req_offset < 0)
+      return fail(MLA_ERR_SEGMENTS, "segment %d has a negative start", i);
+    total += segs[i].length;
+    if (total > INT32_MAX) return fail(MLA_ERR_UNSUPPORTED, "more than 2^31-1 rows");
+  }
+  for (int pass = 0; pass < 2; ++pass) {
+    std::vector<int32_t> idx(n);
+    std::iota(idx.begin(), idx.end(), 0);
+    auto key = [&](int32_t i) { return pass == 0 ? segs[i].kv_start : segs[i].req_offset; };
+    std::sort(idx.begin(), idx.end(), [&](int32_t x, int32_t y) { return key(x) < key(y); });
+    int64_t at = 0;
+    for (int32_t i : idx) {
+      if (key(i) != at)
+        return fail(MLA_ERR_SEGMENTS, "segments do not tile [0, %lld) in %s space at %lld (segment %d)",
+                    (long long)total, pass == 0 ? "storage" : "request", (long long)at, i);
+      at += segs[i].length;
+    }
+  }
+  *n_rows = total;
+  return MLA_OK;
+}
+
+mla_status check_prot(const int32_t* prot, int32_t n_prot, int64_t n_rows) {
+  if (n_prot < 0) return fail(MLA_ERR_ROWS, "n_prot = %d", n_prot);
+  if (n_prot > 0 && prot == nullptr) return fail(MLA_ERR_NULL, "prot_rows is NULL");
+  if (n_prot > n_rows) return fail(MLA_ERR_ROWS, "n_prot %d exceeds n_rows %lld", n_prot, (long long)n_rows);
+  for (int32_t a = 0; a < n_prot; ++a) {
+    if (prot[a] < 0 || prot[a] >= n_rows) return fail(MLA_ERR_ROWS, "prot_rows[%d] = %d out of range", a, prot[a]);
+    if (a > 0 && prot[a] <= prot[a - 1])
+      return fail(MLA_ERR_ROWS, "prot_rows not strictly increasing at %d", a);
+  }
+  return MLA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// plan
+// ---------------------------------------------------------------------------
+struct Plan {
+  mla::PlanHeader hdr{};
+  std::vector<unsigned char> blob;   // exact workspace image
+};
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+mla_status build_plan(const mla_geom* g, const mla_segment* segs, int32_t n_segs, const int32_t* prot,
+                      int32_t n_prot, int64_t split_keys, bool want_blob, Plan* out) {
+  mla_status st = check_geom(g, false);
+  if (st != MLA_OK) return st;
+  int64_t N = 0;
+  if ((st = check_segments(segs, n_segs, &N)) != MLA_OK) return st;
+  if ((st = check_prot(prot, n_prot, N)) != MLA_OK) return st;
+  if (split_keys < 0) return fail(MLA_ERR_SHAPE, "split_keys = %lld must be >= 0", (long long)split_keys);
+
+  const int G = g->n_groups, hpg = g->n_heads / g->n_groups;
+  const int64_t Lh = (int64_t)G * (hpg - 1);
+
+  // request order and storage order
+  std::vector<int32_t> rank_seg(n_segs), storage(n_segs), rank_of(n_segs);
+  std::iota(rank_seg.begin(), rank_seg.end(), 0);
+  std::sort(rank_seg.begin(), rank_seg.end(),
+            [&](int32_t x, int32_t y) { return segs[x].req_offset < segs[y].req_offset; });
+  for (int32_t r = 0; r < n_segs; ++r) rank_of[rank_seg[r]] = r;
+  std::iota(storage.begin(), storage.end(), 0);
+  std::sort(storage.begin(), storage.end(),
+            [&](int32_t x, int32_t y) { return segs[x].kv_start < segs[y].kv_start; });
+
+  // chunks of each segment's visible list (ranks 0 .. rank(s))
+  std::vector<mla::SegInfo> info(n_segs);
+  std::vector<mla::ChunkInfo> chunks;
+  for (int32_t s = 0; s < n_segs; ++s) {
+    info[s].kv_start = segs[s].kv_start;
+    info[s].length = segs[s].length;
+    info[s].req_offset = segs[s].req_offset;
+    info[s].rank = rank_of[s];
+    info[s].chunk_off = (int32_t)chunks.size();
+    int32_t first = 0;
+    int64_t keys = 0;
+    for (int32_t r = 0; r <= rank_of[s]; ++r) {
+      const int64_t len = segs[rank_seg[r]].length;
+      const bool close = split_keys == 0 ? (r > first) : (r > first && keys + len > split_keys);
+      if (close) {
+        chunks.push_back({first, r - 1});
+        first = r;
+        keys = 0;
+      }
+      keys += len;
+    }
+    chunks.push_back({first, rank_of[s]});
+    info[s].n_chunks = (int32_t)chunks.size() - info[s].chunk_off;
+  }
+
+  // partial counts: global slots in storage order, then local slots
+  int64_t cum = 0;
+  for (int32_t i : storage) {
+    info[i].cum_global = cum;
+    cum += (int64_t)G * info[i].length * info[i].n_chunks;
+  }
+  const int64_t global_parts = cum;
+  std::vector<int32_t> prot_seg(n_prot);
+  std::vector<int64_t> cum_local(n_prot + 1, 0);
+  {
+    int32_t si = 0;
+    for (int32_t a = 0; a < n_prot; ++a) {
+      while (segs[storage[si]].kv_start + segs[storage[si]].length <= prot[a]) ++si;
+      prot_seg[a] = storage[si];
+      cum_local[a + 1] = cum_local[a] + Lh * info[storage[si]].n_chunks;
+    }
+  }
+  const int64_t n_slots = N * G + (int64_t)n_prot * Lh;
+  const int64_t n_parts = global_parts + cum_local[n_prot];
+
+  // work items: per segment, its rows' head-rows in runs of 64, times its chunks
+  struct Cand {
+    mla::WorkItem w;
+    int64_t cost;
+  };
+  std::vector<Cand> items;
+  auto add_items = [&](int kind, int32_t s, int64_t hr_lo, int64_t hr_hi, auto row_of) {
+    for (int64_t h = hr_lo; h < hr_hi; h += mla::kTileRows) {
+      const int64_t cnt = std::min<int64_t>(mla::kTileRows, hr_hi - h);
+      const int64_t max_u = row_of(h + cnt - 1) - segs[s].kv_start;
+      for (int32_t c = 0; c < info[s].n_chunks; ++c) {
+        const mla::ChunkInfo ch = chunks[info[s].chunk_off + c];
+        int64_t tiles = 0;
+        for (int32_t r = ch.first_rank; r <= ch.last_rank; ++r) {
+          const int32_t t = rank_seg[r];
+          const int64_t keys = t == s ? max_u + 1 : segs[t].length;
+          tiles += (keys + 63) / 64;
+        }
+        Cand cd;
+        cd.w.hr_begin = h;
+        cd.w.count = (int32_t)cnt;
+        cd.w.kind = kind;
+        cd.w.seg = s;
+        cd.w.chunk = c;
+        cd.w.max_u = (int32_t)max_u;
+        cd.w.pad = 0;
+        cd.cost = tiles * ((cnt + 31) / 32);
+        items.push_back(cd);
+      }
+    }
+  };
+  for (int32_t s = 0; s < n_segs; ++s)
+    add_items(0, s, segs[s].kv_start * G, (segs[s].kv_start + segs[s].length) * G,
+              [&](int64_t hr) { return hr / G; });
+  if (Lh > 0) {
+    int32_t a = 0;
+    while (a < n_prot) {
+      const int32_t s = prot_seg[a];
+      int32_t b = a;
+      while (b < n_prot && prot_seg[b] == s) ++b;
+      add_items(1, s, a * Lh, (int64_t)b * Lh, [&](int64_t hr) { return (int64_t)prot[hr / Lh]; });
+      a = b;
+    }
+  }
+  // longest first; ties in a fixed order
+  std::stable_sort(items.begin(), items.end(), [](const Cand& x, const Cand& y) { return x.cost > y.cost; });
+  if (items.size() > (size_t)INT32_MAX - 256) return fail(MLA_ERR_UNSUPPORTED, "too many work items");
+
+  // layout of the workspace image
+  mla::PlanHeader& h = out->hdr;
+  h = mla::PlanHeader{};
+  h.n_rows = N;
+  h.n_slots = n_slots;
+  h.n_parts = n_parts;
+  h.global_parts = global_parts;
+  h.n_segs = n_segs;
+  h.n_items = (int32_t)items.size();
+  h.n_prot = n_prot;
+  size_t off = align_up(sizeof(mla::PlanHeader), 256);
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, 256);
+    return (int64_t)o;
+  };
+  h.off_segs = take(sizeof(mla::SegInfo) * n_segs);
+  h.off_rank = take(sizeof(int32_t) * n_segs);
+  h.off_storage = take(sizeof(int32_t) * n_segs);
+  h.off_chunks = take(sizeof(mla::ChunkInfo) * chunks.size());
+  h.off_items = take(sizeof(mla::WorkItem) * items.size());
+  h.off_prot = take(sizeof(int32_t) * std::max<int32_t>(n_prot, 1));
+  h.off_prot_seg = take(sizeof(int32_t) * std::max<int32_t>(n_prot, 1));
+  h.off_cum_local = take(sizeof(int64_t) * (n_prot + 1));
+  h.off_theta = take(sizeof(double) * mla::kMaxRopePairs);
+  h.total_bytes = (int64_t)off;
+  if (!want_blob) return MLA_OK;
+
+  out->blob.assign(off, 0);
+  unsigned char* B = out->blob.data();
+  std::memcpy(B, &h, sizeof h);
+  std::memcpy(B + h.off_segs, info.data(), sizeof(mla::SegInfo) * n_segs);
+  std::memcpy(B + h.off_rank, rank_seg.data(), sizeof(int32_t) * n_segs);
+  std::memcpy(B + h.off_storage, storage.data(), sizeof(int32_t) * n_segs);
+  std::memcpy(B + h.off_chunks, chunks.data(), sizeof(mla::ChunkInfo) * chunks.size());
+  mla::WorkItem* wi = reinterpret_cast<mla::WorkItem*>(B + h.off_items);
+  for (size_t i = 0; i < items.size(); ++i) wi[i] = items[i].w;
+  if (n_prot > 0) {
+    std::memcpy(B + h.off_prot, prot, sizeof(int32_t) * n_prot);
+    std::memcpy(B + h.off_prot_seg, prot_seg.data(), sizeof(int32_t) * n_prot);
+  }
+  std::memcpy(B + h.off_cum_local, cum_local.data(), sizeof(int64_t) * (n_prot + 1));
+  double* th = reinterpret_cast<double*>(B + h.off_theta);
+  const double two_pi = 6.283185307179586476925286766559;
+  for (int j = 0; j < g->d_rope / 2; ++j)
+    th[j] = std::pow(g->rope_base, -2.0 * j / g->d_rope) / two_pi;
+  return MLA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// pinned staging for the plan upload: two slots per device, each reused only
+// after the copy that last read it has completed
+// ---------------------------------------------------------------------------
+struct Staging {
+  void* host[2] = {nullptr, nullptr};
+  size_t cap[2] = {0, 0};
+  hipEvent_t done[2] = {nullptr, nullptr};
+  int next = 0;
+};
+std::mutex g_stage_mu;
+std::map<int, Staging> g_stage;
+
+mla_status upload_plan(const Plan& plan, void* ws, hipStream_t stream) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lk(g_stage_mu);
+  Staging& st = g_stage[dev];
+  const int k = st.next;
+  st.next ^= 1;
+  if (st.done[k] == nullptr) {
+    if ((e = hipEventCreateWithFlags(&st.done[k], hipEventDisableTiming)) != hipSuccess)
+      return hip_fail(e, "hipEventCreateWithFlags");
+  } else if ((e = hipEventSynchronize(st.done[k])) != hipSuccess) {
+    return hip_fail(e, "hipEventSynchronize (staging)");
+  }
+  const size_t bytes = plan.blob.size();
+  if (st.cap[k] < bytes) {
+    if (st.host[k] != nullptr) (void)hipHostFree(st.host[k]);
+    st.host[k] = nullptr;
+    st.cap[k] = 0;
+    const size_t cap = std::max<size_t>(bytes, 1 << 20);
+    if ((e = hipHostMalloc(&st.host[k], cap, hipHostMallocDefault)) != hipSuccess)
+      return hip_fail(e, "hipHostMalloc (plan staging)");
+    st.cap[k] = cap;
+  }
+  std::memcpy(st.host[k], plan.blob.data(), bytes);
+  if ((e = hipMemcpyAsync(ws, st.host[k], bytes, hipMemcpyHostToDevice, stream)) != hipSuccess)
+    return hip_fail(e, "hipMemcpyAsync (plan upload)");
+  if ((e = hipEventRecord(st.done[k], stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  return MLA_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+const char* mla_status_str(mla_status s) {
+  switch (s) {
+    case MLA_OK: return "MLA_OK";
+    case MLA_ERR_NULL: return "MLA_ERR_NULL: a required pointer is NULL";
+    case MLA_ERR_SHAPE: return "MLA_ERR_SHAPE: inconsistent sizes, alignment or geometry";
+    case MLA_ERR_UNSUPPORTED: return "MLA_ERR_UNSUPPORTED: configuration not built";
+    case MLA_ERR_SEGMENTS: return "MLA_ERR_SEGMENTS: segment table does not tile the rows";
+    case MLA_ERR_ROWS: return "MLA_ERR_ROWS: protected rows unsorted, duplicated or out of range";
+    case MLA_ERR_WORKSPACE: return "MLA_ERR_WORKSPACE: workspace too small";
+    case MLA_ERR_HIP: return "MLA_ERR_HIP: HIP runtime error";
+  }
+  return "unknown mla_status";
+}
+
+const char* mla_last_error_detail(void) { return g_detail.c_str(); }
+
+const char* mla_version(void) { return "mla_online 0.1 (gfx950)"; }
+
+mla_status mla_online_attend_query(const mla_geom* geom, const mla_segment* segs, int32_t n_segs,
+                                   const int32_t* prot_rows, int32_t n_prot, int64_t split_keys,
+                                   int64_t* n_slots, int64_t* n_parts, size_t* ws_bytes) {
+  g_detail.clear();
+  if (n_slots == nullptr || n_parts == nullptr || ws_bytes == nullptr)
+    return fail(MLA_ERR_NULL, "output pointer is NULL");
+  Plan p;
+  const mla_status st = build_plan(geom, segs, n_segs, prot_rows, n_prot, split_keys, false, &p);
+  if (st != MLA_OK) return st;
+  *n_slots = p.hdr.n_slots;
+  *n_parts = p.hdr.n_parts;
+  *ws_bytes = (size_t)p.hdr.total_bytes;
+  return MLA_OK;
+}
+
+mla_status mla_online_attend(const mla_geom* geom, const mla_segment* segs, int32_t n_segs,
+                             const int32_t* prot_rows, int32_t n_prot, int64_t split_keys, const void* kv,
+                             const void* q_glob, const void* q_loc, float* part_o, float* part_lse,
+                             int64_t* part_ptr, int32_t* part_seg, uint8_t* row_src, void* workspace,
+                             size_t ws_bytes, void* stream) {
+  g_detail.clear();
+  Plan p;
+  mla_status st = build_plan(geom, segs, n_segs, prot_rows, n_prot, split_keys, true, &p);
+  if (st != MLA_OK) return st;
+  const int hpg = geom->n_heads / geom->n_groups;
+  if (kv == nullptr || q_glob == nullptr || part_o == nullptr || part_lse == nullptr || part_ptr == nullptr ||
+      workspace == nullptr)
+    return fail(MLA_ERR_NULL, "kv, q_glob, part_o, part_lse, part_ptr and workspace are required");
+  if (n_prot > 0 && hpg > 1 && q_loc == nullptr) return fail(MLA_ERR_NULL, "q_loc is NULL but Local heads exist");
+  if (!aligned16(kv) || !aligned16(q_glob) || (q_loc && !aligned16(q_loc)) || !aligned16(part_o))
+    return fail(MLA_ERR_SHAPE, "kv, q_glob, q_loc and part_o must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return fail(MLA_ERR_SHAPE, "workspace must be 256-byte aligned");
+  if (ws_bytes < (size_t)p.hdr.total_bytes)
+    return fail(MLA_ERR_WORKSPACE, "workspace %zu bytes < required %lld", ws_bytes, (long long)p.hdr.total_bytes);
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if ((st = upload_plan(p, workspace, s)) != MLA_OK) return st;
+
+  mla::AttendArgs a{};
+  a.kv = kv;
+  a.q_glob = q_glob;
+  a.q_loc = q_loc;
+  a.part_o = part_o;
+  a.part_lse = part_lse;
+  a.part_ptr = part_ptr;
+  a.part_seg = part_seg;
+  a.row_src = row_src;
+  a.ws = reinterpret_cast<const unsigned char*>(workspace);
+  a.n_rows = p.hdr.n_rows;
+  a.n_slots = p.hdr.n_slots;
+  a.n_items = p.hdr.n_items;
+  a.n_prot = n_prot;
+  a.n_groups = geom->n_groups;
+  a.n_local = geom->n_groups * (hpg - 1);
+  a.d_latent = geom->d_latent;
+  a.d_rope = geom->d_rope;
+  a.scale_log2 = geom->softmax_scale * 1.4426950408889634f;
+  a.hdr = p.hdr;
+  hipError_t e = mla::launch_plan(a, s);
+  if (e != hipSuccess) return hip_fail(e, "plan kernels");
+  e = mla::launch_attend(a, s);
+  if (e != hipSuccess) return hip_fail(e, "attention kernel");
+  return MLA_OK;
+}
+
+mla_status mla_segment_merge(int64_t n_slots, int32_t d_latent, const float* part_o, const float* part_lse,
+                             const int64_t* part_ptr, int32_t out_dtype, void* out_o, float* out_lse,
+                             void* stream) {
+  g_detail.clear();
+  if (n_slots < 0) return fail(MLA_ERR_SHAPE, "n_slots = %lld", (long long)n_slots);
+  if (d_latent != 512 && d_latent != 64) return fail(MLA_ERR_UNSUPPORTED, "d_latent %d; built: 64, 512", d_latent);
+  if (out_dtype != MLA_BF16 && out_dtype != MLA_F32) return fail(MLA_ERR_SHAPE, "out_dtype %d", out_dtype);
+  if (n_slots == 0) return MLA_OK;
+  if (part_o == nullptr || part_lse == nullptr || part_ptr == nullptr || out_o == nullptr)
+    return fail(MLA_ERR_NULL, "part_o, part_lse, part_ptr and out_o are required");
+  if (!aligned16(part_o) || !aligned16(out_o)) return fail(MLA_ERR_SHAPE, "part_o and out_o must be 16-byte aligned");
+  hipError_t e = mla::launch_merge(n_slots, d_latent, part_o, part_lse, part_ptr, out_dtype, out_o, out_lse,
+                                   reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "merge kernel");
+  return MLA_OK;
+}
+
+mla_status mla_sliced_oproj_add(const mla_geom* geom, int64_t n_rows, const void* o_glob, const void* o_loc,
+                                const int32_t* glob_head, const int32_t* prot_rows, int32_t n_prot,
+                                const void* w_o, const void* z_off, float* z, void* stream) {
+  g_detail.clear();
+  mla_status st = check_geom(geom, true);
+  if (st != MLA_OK) return st;
+  if (n_rows < 1 || n_rows > INT32_MAX) return fail(MLA_ERR_SHAPE, "n_rows = %lld", (long long)n_rows);
+  if (n_prot < 0 || n_prot > n_rows) return fail(MLA_ERR_ROWS, "n_prot = %d with n_rows = %lld", n_prot, (long long)n_rows);
+  const int hpg = geom->n_heads / geom->n_groups;
+  if (glob_head == nullptr) return fail(MLA_ERR_NULL, "glob_head is NULL");
+  for (int g = 0; g < geom->n_groups; ++g)
+    if (glob_head[g] < 0 || glob_head[g] >= hpg)
+      return fail(MLA_ERR_SHAPE, "glob_head[%d] = %d outside [0, %d)", g, glob_head[g], hpg);
+  if (o_glob == nullptr || w_o == nullptr || z == nullptr) return fail(MLA_ERR_NULL, "o_glob, w_o and z are required");
+  if (n_prot > 0 && prot_rows == nullptr) return fail(MLA_ERR_NULL, "prot_rows is NULL");
+  if (n_prot > 0 && hpg > 1 && o_loc == nullptr) return fail(MLA_ERR_NULL, "o_loc is NULL but Local heads exist");
+  if (n_prot < n_rows && z_off == nullptr) return fail(MLA_ERR_NULL, "z_off is NULL but unprotected rows exist");
+  if (!aligned16(o_glob) || (o_loc && !aligned16(o_loc)) || !aligned16(w_o))
+    return fail(MLA_ERR_SHAPE, "o_glob, o_loc and w_o must be 16-byte aligned");
+  mla::OprojArgs a{};
+  a.o_glob = o_glob;
+  a.o_loc = o_loc;
+  a.prot_rows = prot_rows;
+  a.w_o = w_o;
+  a.z_off = z_off;
+  a.z = z;
+  a.n_rows = n_rows;
+  a.n_prot = n_prot;
+  a.n_heads = geom->n_heads;
+  a.n_groups = geom->n_groups;
+  a.d_latent = geom->d_latent;
+  a.d_model = geom->d_model;
+  a.n_pg = geom->n_proj_groups;
+  for (int g = 0; g < geom->n_groups; ++g) a.glob_head[g] = glob_head[g];
+  hipError_t e = mla::launch_oproj(a, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "o-proj kernels");
+  return MLA_OK;
+}
+
+}  // extern "C"

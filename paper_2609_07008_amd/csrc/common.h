@@ -1,0 +1,146 @@
+// Internal declarations shared by the MLA-Online HIP sources (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mla_online.h"
+
+namespace mla {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+#define MLA_LDS __attribute__((address_space(3)))
+
+constexpr int kMaxRopePairs = 32;   // d_rope <= 64
+constexpr int kTileRows = 64;       // head-rows per attention work item (2 blocks of 32)
+constexpr int kMaxGroups = 128;
+
+// ----------------------------------------------------------------------------
+// Plan written by the host into the attend workspace (all offsets in bytes from
+// the workspace base).  Segment "rank" = position in request order.
+// ----------------------------------------------------------------------------
+struct SegInfo {
+  int64_t kv_start;
+  int64_t length;
+  int64_t req_offset;
+  int64_t cum_global;   // global-slot partials before this segment's first row
+  int32_t rank;         // request-order rank
+  int32_t n_chunks;     // chunks of this segment's visible list
+  int32_t chunk_off;    // first entry in the chunk table
+  int32_t pad;
+};
+
+struct ChunkInfo {
+  int32_t first_rank;   // first / last segment rank covered (request order)
+  int32_t last_rank;
+};
+
+// One attention work item: up to 128 consecutive head-rows of q_glob (kind 0,
+// head-row = r*G + g) or of q_loc (kind 1, head-row = a*L_h + k), all of them
+// belonging to rows of segment `seg`, attending to chunk `chunk` of that
+// segment's visible-segment list.
+struct WorkItem {
+  int64_t hr_begin;
+  int32_t count;
+  int32_t kind;
+  int32_t seg;
+  int32_t chunk;
+  int32_t max_u;        // largest canonical offset of the item's rows in `seg`
+  int32_t pad;
+};
+
+struct PlanHeader {
+  int64_t n_rows;
+  int64_t n_slots;
+  int64_t n_parts;
+  int64_t global_parts;   // partials of all Global slots
+  int32_t n_segs;
+  int32_t n_items;
+  int32_t n_prot;
+  int32_t pad;
+  // byte offsets inside the workspace
+  int64_t off_segs;        // SegInfo[n_segs] by segment index
+  int64_t off_rank;        // int32[n_segs]: segment index of each rank
+  int64_t off_storage;     // int32[n_segs]: segment indices sorted by kv_start
+  int64_t off_chunks;      // ChunkInfo[total chunks]
+  int64_t off_items;       // WorkItem[n_items], in launch order
+  int64_t off_prot;        // int32[n_prot]: protected rows
+  int64_t off_prot_seg;    // int32[n_prot]: segment of each protected row
+  int64_t off_cum_local;   // int64[n_prot + 1]: local-slot partials before row a
+  int64_t off_theta;       // double[d_r/2]: base^(-2j/d_r) / (2 pi), RoPE frequency in revolutions
+  int64_t total_bytes;
+};
+
+// ----------------------------------------------------------------------------
+// launchers (defined in the .hip files); all return hipError_t of the launch
+// ----------------------------------------------------------------------------
+struct AttendArgs {
+  const void* kv;
+  const void* q_glob;
+  const void* q_loc;
+  float* part_o;
+  float* part_lse;
+  int64_t* part_ptr;
+  int32_t* part_seg;
+  uint8_t* row_src;
+  const unsigned char* ws;   // device workspace holding the plan
+  int64_t n_rows;
+  int64_t n_slots;
+  int32_t n_items;
+  int32_t n_prot;
+  int32_t n_groups;
+  int32_t n_local;           // L_h = G*(hpg-1)
+  int32_t d_latent;
+  int32_t d_rope;
+  float scale_log2;          // softmax_scale * log2(e)
+  PlanHeader hdr;            // copy of the plan header (offsets)
+};
+
+hipError_t launch_plan(const AttendArgs& a, hipStream_t s);
+hipError_t launch_attend(const AttendArgs& a, hipStream_t s);
+
+hipError_t launch_merge(int64_t n_slots, int32_t d_latent, const float* part_o,
+                        const float* part_lse, const int64_t* part_ptr, int32_t out_dtype,
+                        void* out_o, float* out_lse, hipStream_t s);
+
+struct OprojArgs {
+  const void* o_glob;
+  const void* o_loc;
+  const int32_t* prot_rows;
+  const void* w_o;
+  const void* z_off;
+  float* z;
+  int64_t n_rows;
+  int32_t n_prot;
+  int32_t n_heads;
+  int32_t n_groups;
+  int32_t d_latent;
+  int32_t d_model;
+  int32_t n_pg;
+  int32_t glob_head[kMaxGroups];
+};
+
+hipError_t launch_oproj(const OprojArgs& a, hipStream_t s);
+
+// ----------------------------------------------------------------------------
+// device helpers
+// ----------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  // round-to-nearest-even conversion of two floats into packed bf16
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  bf16x2_t v;
+  v[0] = (__bf16)lo;
+  v[1] = (__bf16)hi;
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
+
+}  // namespace mla

@@ -1,0 +1,211 @@
+// Group-aligned sliced first output projection with artifact restore-and-replace
+// (eq:offonline, eq:factorization, Alg. 2: z_online = W_{a,G} O_G + W_{a,L} O_{L,A};
+// z = z_online + z_off on unprotected rows, z = z_online on protected rows).
+//
+// Two bf16 MFMA GEMM passes per projection group pg, both on the caller's stream:
+//   pass L: rows a of the protected set, K = the Local heads of pg's groups;
+//           the result is written straight into z[prot_rows[a]].
+//   pass G: every row, K = the Global heads of pg's groups; the epilogue adds
+//           z_off[r] on unprotected rows and the pass-L value already in z[r]
+//           on protected rows, so z_off is never read for protected rows.
+// Each head's weight rows are a d_c-row block of w_o[pg]; a K tile of 32 never
+// straddles two heads, so the B operand is gathered per tile by head.
+#include "common.h"
+
+namespace mla {
+
+constexpr int OP_BM = 128, OP_BN = 128, OP_BK = 32;
+constexpr int OP_ALD = OP_BK + 8;     // padded A row (bf16): 80 B, conflict-free b128 reads
+constexpr int OP_BLD = OP_BN + 16;    // padded B row (bf16): 288 B, conflict-free transposed reads
+
+template <int PASS>   // 0 = Local pass over protected rows, 1 = Global pass over all rows
+__global__ __launch_bounds__(256) void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][OP_BM * OP_ALD];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][OP_BK * OP_BLD];
+  __shared__ int row_flag[OP_BM];
+  __shared__ int row_out[OP_BM];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int hpg = a.n_heads / a.n_groups;
+  const int gpp = a.n_groups / a.n_pg;              // output groups per projection group
+  const int cw = a.d_model / a.n_pg;                // channels per projection group
+  const int heads_pp = a.n_heads / a.n_pg;
+  const int DC = a.d_latent;
+
+  int bid = blockIdx.x;
+  const int nt = bid % n_tiles;
+  bid /= n_tiles;
+  const int mt = bid % m_tiles;
+  const int pg = bid / m_tiles;
+  const int m0 = mt * OP_BM, n0 = nt * OP_BN;
+
+  const int64_t M = PASS == 0 ? (int64_t)a.n_prot : a.n_rows;
+  const int heads_k = PASS == 0 ? gpp * (hpg - 1) : gpp;   // d_c-wide K blocks
+  const int K = heads_k * DC;
+  const uint16_t* A = (const uint16_t*)(PASS == 0 ? a.o_loc : a.o_glob);
+  const int64_t lda = PASS == 0 ? (int64_t)a.n_groups * (hpg - 1) * DC : (int64_t)a.n_groups * DC;
+  const int64_t acol = PASS == 0 ? (int64_t)pg * gpp * (hpg - 1) * DC : (int64_t)pg * gpp * DC;
+  const uint16_t* W = (const uint16_t*)a.w_o + (int64_t)pg * heads_pp * DC * cw;
+
+  if (tid < OP_BM) {
+    const int64_t m = m0 + tid;
+    int flag = 0, orow = -1;
+    if (m < M) {
+      if (PASS == 0) {
+        orow = a.prot_rows[m];
+        flag = 1;
+      } else {
+        orow = (int)m;
+        int lo = 0, hi = a.n_prot;          // binary search in the sorted protected rows
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (a.prot_rows[mid] < (int)m) lo = mid + 1; else hi = mid;
+        }
+        flag = (lo < a.n_prot && a.prot_rows[lo] == (int)m) ? 1 : 0;
+      }
+    }
+    row_flag[tid] = flag;
+    row_out[tid] = orow;
+  }
+
+  // weight row of K index k (k is a multiple of 32 inside one head block)
+  auto w_row = [&](int k) -> int64_t {
+    const int kb = k / DC, d = k - kb * DC;
+    int hl;   // head index inside the projection group
+    if (PASS == 0) {
+      const int gl = kb / (hpg - 1), j = kb - gl * (hpg - 1);
+      const int gh = a.glob_head[pg * gpp + gl];
+      hl = gl * hpg + (j < gh ? j : j + 1);
+    } else {
+      hl = kb * hpg + a.glob_head[pg * gpp + kb];
+    }
+    return (int64_t)hl * DC + d;
+  };
+
+  u32x4 ra[2], rb[2];
+  auto load_tiles = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + 256 * i;
+      const int r = c >> 2, cc = c & 3;
+      int64_t m = m0 + r;
+      if (m >= M) m = M - 1;
+      ra[i] = *(const u32x4*)(A + m * lda + acol + k0 + cc * 8);
+    }
+    const int64_t wr = w_row(k0);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + 256 * i;
+      const int kr = c >> 4, cc = c & 15;
+      const int n = n0 + cc * 8;
+      if (n < cw)
+        rb[i] = *(const u32x4*)(W + (wr + kr) * cw + n);
+      else
+        rb[i] = u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto store_tiles = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + 256 * i;
+      *(u32x4*)(&As[buf][(c >> 2) * OP_ALD + (c & 3) * 8]) = ra[i];
+      *(u32x4*)(&Bs[buf][(c >> 4) * OP_BLD + (c & 15) * 8]) = rb[i];
+    }
+  };
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int wm = wave >> 1, wn = wave & 1;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int q = lane >> 4, j16 = lane & 15;
+
+  load_tiles(0);
+  store_tiles(0);
+  __syncthreads();
+  const int nk = K / OP_BK;
+  for (int it = 0; it < nk; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < nk) load_tiles((it + 1) * OP_BK);
+#pragma unroll
+    for (int ks = 0; ks < OP_BK / 16; ++ks) {
+      bf16x8 af[2], bfr[2];
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi)
+        af[mi] = *(const bf16x8*)(&As[buf][(wm * 64 + mi * 32 + l32) * OP_ALD + ks * 16 + half * 8]);
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni) {
+        // transposed LDS reads: lane (r*4+cb) of each 16-lane group addresses
+        // k-row kb+r, columns n+cb*4..; lane j then holds column n+j of rows kb..kb+3
+        const int r = j16 >> 2, cb = j16 & 3;
+        const int kb = ks * 16 + (q >> 1) * 8;
+        const int n = wn * 64 + ni * 32 + (q & 1) * 16 + cb * 4;
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (MLA_LDS bf16x4*)(&Bs[buf][(kb + r) * OP_BLD + n]));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (MLA_LDS bf16x4*)(&Bs[buf][(kb + 4 + r) * OP_BLD + n]));
+        bfr[ni] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bfr[ni], acc[mi][ni], 0, 0, 0);
+    }
+    __syncthreads();
+    if (it + 1 < nk) {
+      store_tiles(buf ^ 1);
+      __syncthreads();
+    }
+  }
+
+  // epilogue: lane holds column l32 of each 32x32 block, rows half*4 + 8i + j
+  const uint16_t* zoff = (const uint16_t*)a.z_off;
+#pragma unroll
+  for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni) {
+      const int n = n0 + wn * 64 + ni * 32 + l32;
+      if (n >= cw) continue;
+      const int64_t ch = (int64_t)pg * cw + n;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int r = wm * 64 + mi * 32 + half * 4 + (e >> 2) * 8 + (e & 3);
+        if (m0 + r >= M) continue;
+        const int64_t orow = row_out[r];
+        float v = acc[mi][ni][e];
+        float* dst = a.z + orow * a.d_model + ch;
+        if (PASS == 1) {
+          if (row_flag[r]) {
+            if (hpg > 1) v += *dst;   // the Local pass wrote this row first
+          } else
+            v += __uint_as_float((uint32_t)zoff[orow * a.d_model + ch] << 16);
+        }
+        *dst = v;
+      }
+    }
+}
+
+hipError_t launch_oproj(const OprojArgs& a, hipStream_t s) {
+  const int cw = a.d_model / a.n_pg;
+  const int n_tiles = (cw + OP_BN - 1) / OP_BN;
+  const int hpg = a.n_heads / a.n_groups;
+  if (a.n_prot > 0 && hpg > 1) {
+    const int m_tiles = (a.n_prot + OP_BM - 1) / OP_BM;
+    oproj_kernel<0><<<dim3((unsigned)(m_tiles * n_tiles * a.n_pg)), dim3(256), 0, s>>>(a, m_tiles, n_tiles);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (a.n_rows > 0) {
+    const int m_tiles = (int)((a.n_rows + OP_BM - 1) / OP_BM);
+    oproj_kernel<1><<<dim3((unsigned)(m_tiles * n_tiles * a.n_pg)), dim3(256), 0, s>>>(a, m_tiles, n_tiles);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mla

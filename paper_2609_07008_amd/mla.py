@@ -1,0 +1,141 @@
+"""ctypes binding of libmla_online.so (argument marshalling only).
+
+Every step runs in the HIP library; PyTorch supplies device memory and the
+stream.  Importing this module loads the library and raises if it is missing
+or cannot be loaded: there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch  # loads the HIP runtime the library binds to
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmla_online.so")
+
+MLA_OK = 0
+MLA_BF16, MLA_F32 = 0, 1
+STATUS = {0: "MLA_OK", 1: "MLA_ERR_NULL", 2: "MLA_ERR_SHAPE", 3: "MLA_ERR_UNSUPPORTED",
+          4: "MLA_ERR_SEGMENTS", 5: "MLA_ERR_ROWS", 6: "MLA_ERR_WORKSPACE", 7: "MLA_ERR_HIP"}
+EXPORTS = ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
+           "mla_status_str", "mla_last_error_detail", "mla_version")
+
+
+class MlaError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{STATUS.get(status, status)}: {detail}")
+        self.status = status
+        self.detail = detail
+
+
+class Geom(ctypes.Structure):
+    _fields_ = [("n_heads", ctypes.c_int32), ("n_groups", ctypes.c_int32), ("d_latent", ctypes.c_int32),
+                ("d_rope", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_proj_groups", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_float), ("rope_base", ctypes.c_double)]
+
+
+class Segment(ctypes.Structure):
+    _fields_ = [("kv_start", ctypes.c_int64), ("length", ctypes.c_int64), ("req_offset", ctypes.c_int64)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_07008_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    GP, SP = ctypes.POINTER(Geom), ctypes.POINTER(Segment)
+    lib.mla_online_attend_query.argtypes = [GP, SP, I32, P, I32, I64, ctypes.POINTER(I64), ctypes.POINTER(I64),
+                                            ctypes.POINTER(SZ)]
+    lib.mla_online_attend.argtypes = [GP, SP, I32, P, I32, I64, P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.mla_segment_merge.argtypes = [I64, I32, P, P, P, I32, P, P, P]
+    lib.mla_sliced_oproj_add.argtypes = [GP, I64, P, P, P, P, I32, P, P, P, P]
+    for f in ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add"):
+        getattr(lib, f).restype = ctypes.c_int
+    lib.mla_status_str.argtypes = [ctypes.c_int]
+    lib.mla_status_str.restype = ctypes.c_char_p
+    lib.mla_last_error_detail.argtypes = []
+    lib.mla_last_error_detail.restype = ctypes.c_char_p
+    lib.mla_version.restype = ctypes.c_char_p
+    return lib
+
+
+LIB = _load()
+
+
+def _check(status: int):
+    if status != MLA_OK:
+        raise MlaError(status, LIB.mla_last_error_detail().decode())
+
+
+def make_geom(g) -> Geom:
+    """Geometry from any object with the fields of mla_geom."""
+    return Geom(int(g.n_heads), int(g.n_groups), int(g.d_latent), int(g.d_rope), int(g.d_model),
+                int(g.n_proj_groups), float(g.softmax_scale), float(g.rope_base))
+
+
+def make_segments(segs) -> ctypes.Array:
+    segs = np.asarray(segs, dtype=np.int64).reshape(-1, 3)
+    arr = (Segment * max(1, segs.shape[0]))()
+    for i, (ks, ln, ro) in enumerate(segs):
+        arr[i] = Segment(int(ks), int(ln), int(ro))
+    return arr, int(segs.shape[0])
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, torch.Tensor):
+        return ctypes.c_void_p(t.data_ptr())
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data_as(ctypes.c_void_p)
+    return ctypes.c_void_p(int(t))
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def attend_query(geom, segs, prot_rows, split_keys: int):
+    """Host-only size query: (n_slots, n_parts, workspace bytes)."""
+    g = make_geom(geom)
+    sarr, ns = make_segments(segs)
+    prot = np.ascontiguousarray(prot_rows, dtype=np.int32)
+    n_slots, n_parts, ws = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_size_t()
+    _check(LIB.mla_online_attend_query(ctypes.byref(g), sarr, ns, _ptr(prot), int(prot.shape[0]),
+                                       int(split_keys), ctypes.byref(n_slots), ctypes.byref(n_parts),
+                                       ctypes.byref(ws)))
+    return n_slots.value, n_parts.value, ws.value
+
+
+def online_attend(geom, segs, prot_rows, split_keys, kv, q_glob, q_loc, part_o, part_lse, part_ptr,
+                  part_seg, row_src, workspace, stream=None):
+    """Relocation + segment-wise attention (mla_online_attend).  Device tensors in,
+    device tensors out; prot_rows is a host int32 array."""
+    g = make_geom(geom)
+    sarr, ns = make_segments(segs)
+    prot = np.ascontiguousarray(prot_rows, dtype=np.int32)
+    _check(LIB.mla_online_attend(ctypes.byref(g), sarr, ns, _ptr(prot), int(prot.shape[0]), int(split_keys),
+                                 _ptr(kv), _ptr(q_glob), _ptr(q_loc), _ptr(part_o), _ptr(part_lse),
+                                 _ptr(part_ptr), _ptr(part_seg), _ptr(row_src), _ptr(workspace),
+                                 workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def segment_merge(n_slots, d_latent, part_o, part_lse, part_ptr, out_dtype, out_o, out_lse, stream=None):
+    _check(LIB.mla_segment_merge(int(n_slots), int(d_latent), _ptr(part_o), _ptr(part_lse), _ptr(part_ptr),
+                                 int(out_dtype), _ptr(out_o), _ptr(out_lse), _stream(stream)))
+
+
+def sliced_oproj_add(geom, n_rows, o_glob, o_loc, glob_head, prot_rows_d, n_prot, w_o, z_off, z, stream=None):
+    g = make_geom(geom)
+    gh = np.ascontiguousarray(glob_head, dtype=np.int32)
+    _check(LIB.mla_sliced_oproj_add(ctypes.byref(g), int(n_rows), _ptr(o_glob), _ptr(o_loc), _ptr(gh),
+                                    _ptr(prot_rows_d), int(n_prot), _ptr(w_o), _ptr(z_off), _ptr(z),
+                                    _stream(stream)))
+
+
+def version() -> str:
+    return LIB.mla_version().decode()
