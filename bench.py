@@ -1,0 +1,187 @@
+"""Benchmark of the MLA-Online step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 5] [--split-keys S]
+
+A step is one pass of the whole path over the 256K-context workload:
+mla_online_attend (plan + relocation + segment-wise attention), mla_segment_merge
+and mla_sliced_oproj_add, with every input already resident in HBM.  Prints one
+JSON line.  `value` is achieved TFLOP/s of attention + o-proj algorithmic work
+over the whole step; `roofline` reports the attention kernel alone against the
+dense bf16 MFMA peak; `cpu_baseline` times the fp64 oracle on a bounded row
+sample on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MLA-Online attn+o-proj TFLOP/s & % bf16 MFMA peak; merged rows/s at 256K"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def algorithmic_work(wl):
+    """Exact algorithmic FLOPs and bytes of the instantiated workload.
+
+    attention: every online head-row at position t scores t+1 keys over
+    d_c + d_r dims and accumulates t+1 latent rows of d_c dims:
+    (t+1) * (2*(d_c+d_r) + 2*d_c) flops.  Global heads run on every row, Local
+    heads on protected rows.  o-proj: 2*d_c*d_model/n_pg flops per head-row.
+    """
+    g = wl.geom
+    pos = np.empty(wl.n_rows, dtype=np.float64)
+    for ks, ln, ro in wl.segs:
+        pos[ks:ks + ln] = ro + np.arange(ln)
+    per_key = 2.0 * g.d_qk + 2.0 * g.d_latent
+    prot = np.asarray(wl.prot_rows, dtype=np.int64)
+    vis_glob = float((pos + 1).sum()) * g.n_groups
+    vis_loc = float((pos[prot] + 1).sum()) * g.n_local
+    flop_attn = (vis_glob + vis_loc) * per_key
+    head_rows = wl.n_rows * g.n_groups + len(prot) * g.n_local
+    flop_oproj = head_rows * 2.0 * g.d_latent * g.d_model / g.n_proj_groups
+    return flop_attn, flop_oproj, head_rows
+
+
+def cpu_baseline(wl, budget_s: float = 20.0):
+    """The fp64 oracle as it stands, timed on a bounded sample of rows of the
+    same workload: rows spread over the context (protected and unprotected)."""
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # noqa: BLE001
+        cores = len(os.sched_getaffinity(0))
+    g = wl.geom
+    rng = np.random.default_rng(7)
+    t0 = time.perf_counter()
+    kv = wl.kv()
+    keys = O.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    w_o = wl.w_o()
+    setup = time.perf_counter() - t0
+    prot = set(np.asarray(wl.prot_rows).tolist())
+    cand = rng.permutation(wl.n_rows)
+    pos = np.empty(wl.n_rows, dtype=np.int64)
+    for ks, ln, ro in wl.segs:
+        pos[ks:ks + ln] = ro + np.arange(ln)
+    per_key = 2.0 * g.d_qk + 2.0 * g.d_latent
+    done_rows, flops, elapsed = 0, 0.0, 0.0
+    t_start = time.perf_counter()
+    for r in cand:
+        r = int(r)
+        zr = wl.z_off(rows=[r])
+        O.reference_rows(wl, [r], z_off={r: zr[0]}, kv=kv, keys=keys, w_o=w_o)
+        heads = g.n_groups + (g.n_local if r in prot else 0)
+        flops += (pos[r] + 1) * per_key * heads + heads * 2.0 * g.d_latent * g.d_model / g.n_proj_groups
+        done_rows += 1
+        elapsed = time.perf_counter() - t_start
+        if elapsed > budget_s:
+            break
+    return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "rows_per_s": done_rows / elapsed,
+            "sample": f"{done_rows} random rows of the same workload (fp64, all online heads of each row, "
+                      f"unfactorized), {elapsed:.1f} s after {setup:.1f} s of key setup"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=5)
+    ap.add_argument("--split-keys", type=int, default=-1,
+                    help="chunking of each row's visible segments; -1 = one chunk per slot")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only: the step is measured on the "
+                                   "full set of heads of one layer on one device"}))
+        sys.exit(2)
+
+    import torch
+    from workloads import make_workload
+    from paper_2609_07008_amd import device_inputs, step
+
+    torch.cuda.set_device(0)
+    wl = make_workload(args.workload)
+    g = wl.geom
+    split = wl.n_rows if args.split_keys < 0 else args.split_keys
+    t0 = time.perf_counter()
+    dev = device_inputs.upload(wl)
+    torch.cuda.synchronize()
+    t_upload = time.perf_counter() - t0
+    st = step.OnlineStep(g, wl.segs, wl.prot_rows, wl.glob_head, split, with_part_seg=False)
+    flop_attn, flop_oproj, head_rows = algorithmic_work(wl)
+
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        st.run(dev["kv"], dev["q_glob"], dev["q_loc"], dev["w_o"], dev["z_off"])
+    torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for k in range(args.steps):
+        e = ev[k]
+        e[0].record(stream)
+        st.attend(dev["kv"], dev["q_glob"], dev["q_loc"])
+        e[1].record(stream)
+        st.merge()
+        e[2].record(stream)
+        st.oproj(dev["w_o"], dev["z_off"])
+        e[3].record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    t_att = np.mean([e[0].elapsed_time(e[1]) for e in ev]) / 1e3
+    t_mrg = np.mean([e[1].elapsed_time(e[2]) for e in ev]) / 1e3
+    t_opj = np.mean([e[2].elapsed_time(e[3]) for e in ev]) / 1e3
+    t_step = np.mean([e[0].elapsed_time(e[3]) for e in ev]) / 1e3
+
+    value = (flop_attn + flop_oproj) / t_step / 1e12
+    att_tflops = flop_attn / t_att / 1e12
+    merge_bytes = st.n_parts * (4 * g.d_latent + 4) + st.n_slots * (2 * g.d_latent + 4)
+    oproj_bytes = (wl.n_rows - wl.n_prot) * g.d_model * 2 + wl.n_rows * g.d_model * 4 + head_rows * g.d_latent * 2
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t_step * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"workload {args.workload}: {wl.name}", "rows": wl.n_rows,
+                   "segments": int(wl.segs.shape[0]), "heads": g.n_heads, "groups": g.n_groups,
+                   "protected_rows": wl.n_prot, "d_latent": g.d_latent, "d_rope": g.d_rope,
+                   "d_model": g.d_model, "proj_groups": g.n_proj_groups, "split_keys": split,
+                   "partials": st.n_parts},
+        "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
+        "merged_rows_per_s": round(wl.n_rows / t_step, 1),
+        "flop_attn": flop_attn,
+        "flop_oproj": flop_oproj,
+        "ms": {"attend": round(t_att * 1e3, 3), "merge": round(t_mrg * 1e3, 3), "oproj": round(t_opj * 1e3, 3),
+               "wall_per_step": round(t_wall / args.steps * 1e3, 3), "upload_s": round(t_upload, 2)},
+        "hbm_gbs": {"merge": round(merge_bytes / t_mrg / 1e9, 1), "oproj_add": round(oproj_bytes / t_opj / 1e9, 1)},
+        "roofline": {"bound": "mfma", "achieved": round(att_tflops, 3), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "kernel": "attend_kernel<512,64> (timed with the plan kernels of mla_online_attend)"},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
