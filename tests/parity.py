@@ -1,0 +1,101 @@
+"""Helpers for the GPU parity tests: run the HIP path through the C ABI and
+compare it with the fp64 oracle on the same seeded inputs."""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import mla_oracle as M
+from workloads import round_bf16
+
+ABS_TOL = 2e-2     # max abs error
+REL_TOL = 1e-2     # max abs error / max |reference|
+
+
+def check(name, got, ref, abs_tol=ABS_TOL, rel_tol=REL_TOL):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
+    assert np.isfinite(got).all(), f"{name}: non-finite output"
+    err = float(np.abs(got - ref).max()) if got.size else 0.0
+    scale = float(np.abs(ref).max()) if ref.size else 0.0
+    rel = err / scale if scale > 0 else err
+    assert err <= abs_tol and rel <= rel_tol, f"{name}: max abs err {err:.3e}, relative {rel:.3e}"
+    return err, rel
+
+
+def run(wl, split_keys, z_off=None, with_part_seg=True, out_dtype=None, inputs=None):
+    """One step on the GPU; returns the OnlineStep (device buffers) and the uploaded inputs."""
+    import torch
+    from paper_2609_07008_amd import device_inputs, mla, step
+    if inputs is None:
+        inputs = device_inputs.upload(wl, z_off=z_off)
+    st = step.OnlineStep(wl.geom, wl.segs, wl.prot_rows, wl.glob_head, split_keys,
+                         with_part_seg=with_part_seg,
+                         out_dtype=mla.MLA_BF16 if out_dtype is None else out_dtype)
+    st.run(inputs["kv"], inputs["q_glob"], inputs["q_loc"], inputs["w_o"], inputs["z_off"])
+    torch.cuda.synchronize()
+    return st, inputs
+
+
+def artifact_bf16(wl):
+    """The tiny workload's artifact, computed by the oracle and rounded to bf16
+    (the values the GPU receives)."""
+    return round_bf16(M.artifact(wl).astype(np.float32)).astype(np.float64)
+
+
+def compare_rows(wl, st, rows, z_off, kv=None, keys=None):
+    """Oracle vs GPU on storage rows `rows`: O and lse of every online head, z_online and z."""
+    g = wl.geom
+    rows = np.asarray(sorted(set(int(r) for r in rows)), dtype=np.int64)
+    if isinstance(z_off, np.ndarray):
+        zmap = z_off
+    else:
+        zr = wl.z_off(rows=rows)
+        zmap = {int(r): zr[i] for i, r in enumerate(rows)}
+    ref = M.reference_rows(wl, rows, z_off=zmap, kv=kv, keys=keys)
+    G, hl, d_c = g.n_groups, g.heads_per_group - 1, g.d_latent
+    N = wl.n_rows
+    gslots = (rows[:, None] * G + np.arange(G)[None, :]).reshape(-1)
+    out_o = st.out_o.float()
+    o_g = out_o[gslots].cpu().numpy().reshape(len(rows), G, d_c)
+    l_g = st.out_lse[gslots].cpu().numpy().reshape(len(rows), G)
+    check("O (Global heads)", o_g, ref.o_glob)
+    check("lse (Global heads)", l_g, ref.lse_glob)
+    if ref.prot_idx:
+        idx = sorted(ref.prot_idx)
+        a = np.array([ref.prot_idx[i] for i in idx])
+        lslots = (N * G + (a[:, None] * G * hl) + np.arange(G * hl)[None, :]).reshape(-1)
+        o_l = out_o[lslots].cpu().numpy().reshape(len(a), G, hl, d_c)
+        l_l = st.out_lse[lslots].cpu().numpy().reshape(len(a), G, hl)
+        check("O (Local heads)", o_l, np.stack([ref.o_loc[i] for i in idx]))
+        check("lse (Local heads)", l_l, np.stack([ref.lse_loc[i] for i in idx]))
+    z = st.z[rows].cpu().numpy().astype(np.float64)
+    prot = np.isin(rows, np.asarray(wl.prot_rows))
+    zoff_rows = np.stack([np.zeros(g.d_model) if p else np.asarray(zmap[int(r)], dtype=np.float64)
+                          for r, p in zip(rows, prot)])
+    check("z_online", z - zoff_rows, ref.z_online)
+    check("z", z, ref.z)
+    return ref
+
+
+def check_bookkeeping(wl, st, split_keys, full_part_seg=True):
+    G, hpg = wl.geom.n_groups, wl.geom.heads_per_group
+    rs, ptr, pseg = M.enumerate_plan(wl.segs, G, hpg, wl.prot_rows, split_keys)
+    assert np.array_equal(st.row_src.cpu().numpy(), rs), "row_src"
+    assert np.array_equal(st.part_ptr.cpu().numpy(), ptr), "part_ptr"
+    if st.part_seg is not None and full_part_seg:
+        assert np.array_equal(st.part_seg.cpu().numpy(), pseg), "part_seg"
+
+
+def boundary_sample(wl, n_extra=8, seed=0):
+    """Rows that stress the path: first and last row of every segment, rows on
+    both sides of segment boundaries in request order, protected and query rows."""
+    rng = np.random.default_rng(seed)
+    rows = set()
+    for ks, ln, _ in wl.segs:
+        rows.update([int(ks), int(ks + ln - 1), int(ks + min(1, ln - 1))])
+    prot = np.asarray(wl.prot_rows)
+    if prot.size:
+        rows.update(int(x) for x in rng.choice(prot, size=min(n_extra, prot.size), replace=False))
+    rows.update(int(x) for x in rng.integers(0, wl.n_rows, size=n_extra))
+    return sorted(rows)

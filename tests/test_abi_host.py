@@ -1,0 +1,167 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads and exports
+every function the header declares, the size query agrees with the oracle's
+enumeration, and every validation failure is reported before any device work."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import mla_oracle as M
+from workloads import make_custom, make_workload
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mla_online.h")
+
+
+@pytest.fixture(scope="module")
+def mla():
+    from paper_2609_07008_amd import mla as m
+    return m
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mla_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(mla):
+    declared = header_functions()
+    assert "mla_online_attend" in declared and "mla_segment_merge" in declared
+    assert "mla_sliced_oproj_add" in declared
+    for name in declared:
+        assert hasattr(mla.LIB, name), name
+    assert set(declared) == set(mla.EXPORTS)
+    assert mla.version().startswith("mla_online")
+
+
+def test_status_strings(mla):
+    for code, name in mla.STATUS.items():
+        assert mla.LIB.mla_status_str(code).decode().startswith(name)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("split", [0, 4096, 10 ** 9])
+def test_size_query_matches_oracle(mla, cfg, split):
+    wl = make_workload(cfg)
+    g = wl.geom
+    if cfg >= 4 and split == 0:
+        # closed form instead of a full enumeration (70M partials at 256K)
+        rank = np.argsort(np.argsort(wl.segs[:, 2]))
+        seg, _, _ = M.row_geometry(wl.segs)
+        n_parts = int((rank[seg] + 1).sum()) * g.n_groups + int((rank[seg[wl.prot_rows]] + 1).sum()) * g.n_local
+        n_slots = wl.n_rows * g.n_groups + wl.n_prot * g.n_local
+    else:
+        _, ptr, _ = M.enumerate_plan(wl.segs, g.n_groups, g.heads_per_group, wl.prot_rows, split)
+        n_slots, n_parts = ptr.shape[0] - 1, int(ptr[-1])
+    s, p, ws = mla.attend_query(g, wl.segs, wl.prot_rows, split)
+    assert (s, p) == (n_slots, n_parts)
+    assert ws > 0 and ws % 256 == 0
+
+
+def _tiny():
+    return make_custom([5, 9], req_perm=[1, 0], tq=3, H=4, G=2, d_c=64, d_r=16, d_model=64, seed=3)
+
+
+class _G:
+    def __init__(self, **kw):
+        self.__dict__.update(kw)
+
+
+def _geom(wl, **over):
+    g = wl.geom
+    d = dict(n_heads=g.n_heads, n_groups=g.n_groups, d_latent=g.d_latent, d_rope=g.d_rope, d_model=g.d_model,
+             n_proj_groups=g.n_proj_groups, softmax_scale=g.softmax_scale, rope_base=g.rope_base)
+    d.update(over)
+    return _G(**d)
+
+
+@pytest.mark.parametrize("case,status", [
+    ("heads_not_multiple", "MLA_ERR_SHAPE"),
+    ("dims_unsupported", "MLA_ERR_UNSUPPORTED"),
+    ("bad_scale", "MLA_ERR_SHAPE"),
+    ("gap_in_storage", "MLA_ERR_SEGMENTS"),
+    ("overlap_in_request", "MLA_ERR_SEGMENTS"),
+    ("zero_length", "MLA_ERR_SEGMENTS"),
+    ("no_segments", "MLA_ERR_SEGMENTS"),
+    ("unsorted_prot", "MLA_ERR_ROWS"),
+    ("duplicate_prot", "MLA_ERR_ROWS"),
+    ("prot_out_of_range", "MLA_ERR_ROWS"),
+    ("negative_split", "MLA_ERR_SHAPE"),
+])
+def test_size_query_rejects(mla, case, status):
+    wl = _tiny()
+    geom, segs, prot, split = _geom(wl), wl.segs.copy(), np.asarray(wl.prot_rows).copy(), 0
+    if case == "heads_not_multiple":
+        geom = _geom(wl, n_heads=5)
+    elif case == "dims_unsupported":
+        geom = _geom(wl, d_latent=128, d_rope=32)
+    elif case == "bad_scale":
+        geom = _geom(wl, softmax_scale=float("nan"))
+    elif case == "gap_in_storage":
+        segs[1, 0] += 1
+    elif case == "overlap_in_request":
+        segs[0, 2] = segs[1, 2]
+    elif case == "zero_length":
+        segs[0, 1] = 0
+    elif case == "no_segments":
+        segs = segs[:0]
+    elif case == "unsorted_prot":
+        prot = prot[::-1].copy()
+    elif case == "duplicate_prot":
+        prot = np.concatenate([prot[:1], prot])
+    elif case == "prot_out_of_range":
+        prot = np.concatenate([prot, [wl.n_rows]])
+    elif case == "negative_split":
+        split = -1
+    with pytest.raises(mla.MlaError) as ei:
+        mla.attend_query(geom, segs, prot, split)
+    assert mla.STATUS[ei.value.status] == status, ei.value
+
+
+def test_attend_rejects_before_device_work(mla):
+    """Validation failures of mla_online_attend need no GPU: they return before
+    any HIP call (here: NULL device pointers, misaligned pointers, short workspace)."""
+    wl = _tiny()
+    g = mla.make_geom(wl.geom)
+    sarr, ns = mla.make_segments(wl.segs)
+    prot = np.ascontiguousarray(wl.prot_rows, dtype=np.int32)
+    P = ctypes.c_void_p
+    _, _, ws = mla.attend_query(wl.geom, wl.segs, prot, 0)
+
+    def call(kv, qg, ql, po, pl, pp, wsp, wsb):
+        return mla.LIB.mla_online_attend(ctypes.byref(g), sarr, ns, prot.ctypes.data_as(P), len(prot), 0,
+                                         P(kv), P(qg), P(ql), P(po), P(pl), P(pp), None, None, P(wsp), wsb, None)
+    ok = 1 << 20
+    assert call(0, ok, ok, ok, ok, ok, ok, ws) == 1          # MLA_ERR_NULL
+    assert call(ok, ok, 0, ok, ok, ok, ok, ws) == 1          # q_loc missing with Local heads
+    assert call(ok + 8, ok, ok, ok, ok, ok, ok, ws) == 2     # misaligned kv
+    assert call(ok, ok, ok, ok, ok, ok, ok + 16, ws) == 2    # workspace not 256-byte aligned
+    assert call(ok, ok, ok, ok, ok, ok, ok, ws - 256) == 6   # MLA_ERR_WORKSPACE
+    assert "workspace" in mla.LIB.mla_last_error_detail().decode()
+
+
+def test_merge_and_oproj_reject(mla):
+    P = ctypes.c_void_p
+    assert mla.LIB.mla_segment_merge(4, 128, P(1 << 20), P(1 << 20), P(1 << 20), 0, P(1 << 20), None, None) == 3
+    assert mla.LIB.mla_segment_merge(4, 512, None, P(1 << 20), P(1 << 20), 0, P(1 << 20), None, None) == 1
+    assert mla.LIB.mla_segment_merge(4, 512, P(1 << 20), P(1 << 20), P(1 << 20), 7, P(1 << 20), None, None) == 2
+    assert mla.LIB.mla_segment_merge(0, 512, None, None, None, 0, None, None, None) == 0   # nothing to do
+    wl = _tiny()
+    gh = np.asarray(wl.glob_head, dtype=np.int32)
+    g = mla.make_geom(wl.geom)
+    a = P(1 << 20)
+
+    def call(geom, n_rows, gh_arr, n_prot, zoff):
+        return mla.LIB.mla_sliced_oproj_add(ctypes.byref(geom), n_rows, a, a, gh_arr.ctypes.data_as(P), a, n_prot,
+                                            a, zoff, a, None)
+    assert call(g, 0, gh, 0, a) == 2                                      # no rows
+    assert call(g, wl.n_rows, gh, wl.n_rows + 1, a) == 5                  # more protected rows than rows
+    bad = gh.copy()
+    bad[0] = wl.geom.heads_per_group
+    assert call(g, wl.n_rows, bad, 2, a) == 2                             # Global head outside its group
+    assert call(g, wl.n_rows, gh, 2, None) == 1                           # z_off needed
+    g2 = mla.make_geom(_geom(wl, d_model=40, n_proj_groups=2))
+    assert call(g2, wl.n_rows, gh, 2, a) == 3                             # 20 channels per group

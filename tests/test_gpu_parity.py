@@ -1,0 +1,271 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Tolerances (bf16 inputs, fp32 accumulation): on each of O, lse, z_online and z,
+max abs error <= 2e-2 and max abs error / max |reference| <= 1e-2.  Integer
+bookkeeping (row_src, part_ptr, part_seg) must be bit-exact.
+"""
+import numpy as np
+import pytest
+
+from oracle import mla_oracle as M
+from workloads import make_custom, make_workload, round_bf16
+
+from parity import artifact_bf16, boundary_sample, check, check_bookkeeping, compare_rows, run
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    from paper_2609_07008_amd import mla  # noqa: F401  (fails loudly if the library is missing)
+    yield
+
+
+# ----------------------------------------------------------------------------
+# tiny exactness workload: every row, every head, three split modes
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("variant", ["default", "peaked"])
+@pytest.mark.parametrize("split", [0, 128, 10 ** 9])
+def test_tiny_workload(variant, split):
+    wl = make_workload(1, variant)
+    z_off = artifact_bf16(wl)
+    st, _ = run(wl, split, z_off=z_off)
+    check_bookkeeping(wl, st, split)
+    compare_rows(wl, st, np.arange(wl.n_rows), z_off)
+
+
+# ----------------------------------------------------------------------------
+# 512+64 latent on small custom requests: ragged segments, permuted offsets
+# ----------------------------------------------------------------------------
+CUSTOM = {
+    "ragged": dict(doc_lens=[1, 2, 63, 64, 65, 130, 7], req_perm=[4, 0, 6, 2, 5, 1, 3], tq=37, H=16, G=2,
+                   d_model=256, prot_frac=0.1),
+    "dense_proj": dict(doc_lens=[70, 33, 128], req_perm=[2, 0, 1], tq=20, H=16, G=2, d_model=256, n_pg=1,
+                       prot_frac=0.15),
+    "wide_groups": dict(doc_lens=[96, 40], req_perm=[1, 0], tq=9, H=32, G=4, d_model=512, prot_frac=0.2),
+    "single_segment": dict(doc_lens=[200], req_perm=None, tq=0, H=8, G=1, d_model=128, prot_frac=0.3),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CUSTOM))
+@pytest.mark.parametrize("split", [0, 100, 10 ** 9])
+@pytest.mark.parametrize("peaked", [False, True])
+def test_custom_512(name, split, peaked):
+    kw = dict(CUSTOM[name])
+    std = None
+    if peaked:
+        std = dict(c=1.0, kr=1.0, qc=1.0, qr=1.0, wo=0.02, zoff=0.05)
+    wl = make_custom(d_c=512, d_r=64, seed=100 + sorted(CUSTOM).index(name), fp32=False, std=std, **kw)
+    st, _ = run(wl, split)
+    check_bookkeeping(wl, st, split)
+    z_off = wl.z_off()
+    compare_rows(wl, st, np.arange(wl.n_rows), z_off)
+
+
+@pytest.mark.parametrize("case", ["no_protected", "all_protected", "all_global"])
+def test_edge_cases(case):
+    kw = dict(doc_lens=[65, 3, 64], req_perm=[1, 2, 0], tq=5, d_c=512, d_r=64, fp32=False, seed=21)
+    if case == "no_protected":
+        wl = make_custom(H=16, G=2, d_model=256, prot_rows=np.zeros(0, dtype=np.int32), **kw)
+    elif case == "all_protected":
+        wl = make_custom(H=16, G=2, d_model=256, prot_rows=np.arange(137), **kw)
+    else:
+        wl = make_custom(H=4, G=4, d_model=128, prot_frac=0.2, **kw)   # one head per group: no Local heads
+    z_off = wl.z_off()
+    if case == "all_protected":
+        z_off = np.full_like(z_off, np.nan)        # replaced everywhere: must never be read
+    st, _ = run(wl, 0, z_off=z_off)
+    check_bookkeeping(wl, st, 0)
+    compare_rows(wl, st, np.arange(wl.n_rows), z_off)
+
+
+# ----------------------------------------------------------------------------
+# relocation and visibility: planted needles
+# ----------------------------------------------------------------------------
+def _needle_workload(seed=31):
+    wl = make_custom([70, 90, 66], req_perm=[2, 0, 1], tq=12, H=16, G=2, d_c=512, d_r=64, d_model=256,
+                     fp32=False, seed=seed, prot_frac=0.1)
+    return wl
+
+
+def _plant(wl, kv, row, head_g, seg_idx, u, logit):
+    """Make key u of segment seg_idx score `logit` (natural units) above zero
+    for Global head head_g of `row`, through the RoPE part only, and give it a
+    distinctive latent."""
+    g = wl.geom
+    _, _, pos = M.row_geometry(wl.segs)
+    q = wl.q_glob(rows=[row])[0, head_g]
+    ks, ln, ps = wl.segs[seg_idx]
+    qr = q[g.d_latent:].astype(np.float64)
+    j = int(ks + u)
+    kv = kv.copy()
+    kv[j, : g.d_latent] = 0.0
+    kv[j, 0] = 3.0
+    kv[j, g.d_latent:] = logit / g.softmax_scale * M.rope(qr, int(pos[row]) - int(ps), g.rope_base) / (qr @ qr)
+    return round_bf16(kv.astype(np.float32)), j
+
+
+def _run_with_kv(wl, kv_vals):
+    import torch
+    from paper_2609_07008_amd import device_inputs, step
+    inputs = device_inputs.upload(wl)
+    inputs["kv"] = device_inputs.to_bf16(kv_vals)
+    st = step.OnlineStep(wl.geom, wl.segs, wl.prot_rows, wl.glob_head, 0)
+    st.run(inputs["kv"], inputs["q_glob"], inputs["q_loc"], inputs["w_o"], inputs["z_off"])
+    torch.cuda.synchronize()
+    return st
+
+
+@pytest.mark.parametrize("logit,restart", [(25.0, False), (50.0, True)])
+def test_needle_relocation(logit, restart):
+    """A key planted in an earlier, relocated document dominates the row that
+    sees it.  At +50 nats the tile max passes the first tile's softmax reference
+    by more than 2^64 (44.4 nats), which exercises the kernel's restart path."""
+    wl = _needle_workload()
+    g = wl.geom
+    row = wl.n_rows - 1
+    seg_idx = int(np.argsort(wl.segs[:, 2])[1])        # second document in request order
+    kv, j = _plant(wl, wl.kv(), row, 0, seg_idx, 41, logit)
+    st = _run_with_kv(wl, kv)
+    keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    # scores of the target head without the needle: the restart condition holds iff
+    # the needle exceeds every other score (hence the first tile's max) by > 64 log2 units
+    _, _, pos = M.row_geometry(wl.segs)
+    q = wl.q_glob(rows=[row])[0, 0].astype(np.float64)
+    t = int(pos[row])
+    qt = np.concatenate([q[:g.d_latent], M.rope(q[g.d_latent:], t, g.rope_base)])
+    sc = g.softmax_scale * (keys.k[: t + 1] @ qt)
+    needle = int(np.argmax(sc))
+    others = np.delete(sc, needle).max()
+    assert (sc[needle] - others > 64 * np.log(2.0)) == restart
+    o = st.out_o.float()[row * g.n_groups].cpu().numpy()
+    assert abs(o[0] - 3.0) < 0.05 and np.abs(o[1:]).max() < 0.05
+    compare_rows(wl, st, [row, row - 1, 0, int(wl.segs[seg_idx, 0]) + 41], wl.z_off(), kv=kv, keys=keys)
+
+
+def test_needle_in_the_future_is_invisible():
+    """The needle sits one request position after `row`: `row` cannot see it,
+    the next row (for whose query it is aimed) is dominated by it."""
+    wl = _needle_workload()
+    g = wl.geom
+    s_last = int(np.argsort(wl.segs[:, 2])[2])
+    ks, ln, ps = wl.segs[s_last]
+    row = int(ks + 10)
+    kv, j = _plant(wl, wl.kv(), row + 1, 0, s_last, 11, 25.0)
+    st_a = _run_with_kv(wl, wl.kv())
+    st_b = _run_with_kv(wl, kv)
+    a = st_a.out_o.float()[row * g.n_groups: (row + 1) * g.n_groups].cpu().numpy()
+    b = st_b.out_o.float()[row * g.n_groups: (row + 1) * g.n_groups].cpu().numpy()
+    assert np.array_equal(a, b)
+    c = st_b.out_o.float()[(row + 1) * g.n_groups].cpu().numpy()
+    assert abs(c[0] - 3.0) < 0.05 and np.abs(c[1:]).max() < 0.05
+
+
+# ----------------------------------------------------------------------------
+# merge and o-proj entry points on their own
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("d_c", [64, 512])
+@pytest.mark.parametrize("out_f32", [True, False])
+def test_segment_merge(d_c, out_f32):
+    import torch
+    from paper_2609_07008_amd import mla
+    rng = np.random.default_rng(5)
+    counts = rng.integers(1, 9, size=1001)
+    ptr = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
+    n_parts = int(ptr[-1])
+    po = rng.standard_normal((n_parts, d_c)).astype(np.float32)
+    pl = (rng.standard_normal(n_parts) * 20).astype(np.float32)
+    out = torch.empty((len(counts), d_c), dtype=torch.float32 if out_f32 else torch.bfloat16, device="cuda")
+    lse = torch.empty((len(counts),), dtype=torch.float32, device="cuda")
+    mla.segment_merge(len(counts), d_c, torch.from_numpy(po).cuda(), torch.from_numpy(pl).cuda(),
+                      torch.from_numpy(ptr).cuda(), mla.MLA_F32 if out_f32 else mla.MLA_BF16, out, lse)
+    torch.cuda.synchronize()
+    ref_o = np.zeros((len(counts), d_c))
+    ref_l = np.zeros(len(counts))
+    for s in range(len(counts)):
+        ref_o[s], ref_l[s] = M.lse_merge(po[ptr[s]:ptr[s + 1]], pl[ptr[s]:ptr[s + 1]])
+    got = out.float().cpu().numpy()
+    check("merged O", got, ref_o, abs_tol=2e-2 if not out_f32 else 1e-5, rel_tol=1e-2 if not out_f32 else 1e-5)
+    check("merged lse", lse.cpu().numpy(), ref_l, abs_tol=1e-4, rel_tol=1e-5)
+    single = counts == 1
+    if out_f32:
+        assert np.array_equal(got[single], po[ptr[:-1][single]])
+
+
+@pytest.mark.parametrize("n_pg_dense", [False, True])
+def test_sliced_oproj_alone(n_pg_dense):
+    import torch
+    from paper_2609_07008_amd import device_inputs, mla
+    wl = make_custom([300, 211], req_perm=[1, 0], tq=30, H=16, G=2, d_c=512, d_r=64, d_model=256,
+                     n_pg=1 if n_pg_dense else None, fp32=False, seed=9, prot_frac=0.1)
+    g = wl.geom
+    rng = np.random.default_rng(3)
+    N, P, G, hl = wl.n_rows, wl.n_prot, g.n_groups, g.heads_per_group - 1
+    og = round_bf16(rng.standard_normal((N, G, g.d_latent)).astype(np.float32))
+    ol = round_bf16(rng.standard_normal((P, G, hl, g.d_latent)).astype(np.float32))
+    w_o = wl.w_o()
+    z_off = wl.z_off()
+    zpois = z_off.copy()
+    zpois[wl.prot_rows] = np.nan
+    z = torch.empty((N, g.d_model), dtype=torch.float32, device="cuda")
+    mla.sliced_oproj_add(g, N, device_inputs.to_bf16(og), device_inputs.to_bf16(ol), wl.glob_head,
+                         torch.from_numpy(np.asarray(wl.prot_rows, dtype=np.int32)).cuda(), P,
+                         device_inputs.to_bf16(w_o), device_inputs.to_bf16(zpois), z)
+    torch.cuda.synchronize()
+    blocks = M.dense_blocks(w_o, g.n_heads, g.d_latent, g.d_model)
+    gid, lid = wl.global_head_ids(), wl.local_head_ids().reshape(-1)
+    prot_idx = {int(r): i for i, r in enumerate(wl.prot_rows)}
+    ref = np.zeros((N, g.d_model))
+    for r in range(N):
+        ref[r] = M.project(og[r], gid, blocks)
+        if r in prot_idx:
+            ref[r] += M.project(ol[prot_idx[r]].reshape(-1, g.d_latent), lid, blocks)
+        else:
+            ref[r] += z_off[r]
+    check("z", z.cpu().numpy(), ref, abs_tol=1e-3, rel_tol=1e-4)
+
+
+# ----------------------------------------------------------------------------
+# the five workloads at full size, in the launch configuration of the benchmark
+# ----------------------------------------------------------------------------
+def _big_sample(wl, n_seg=6, seed=1):
+    rng = np.random.default_rng(seed)
+    order = np.argsort(wl.segs[:, 2])
+    pick = list(order[:2]) + list(order[-2:]) + list(rng.choice(order, size=n_seg, replace=False))
+    rows = set()
+    for s in pick:
+        ks, ln, _ = wl.segs[s]
+        rows.update([int(ks), int(ks + ln - 1)])
+    prot = np.asarray(wl.prot_rows)
+    rows.update(int(x) for x in rng.choice(prot, size=6, replace=False))
+    rows.update(int(x) for x in rng.integers(0, wl.n_rows, size=4))
+    return sorted(rows)
+
+
+@pytest.mark.parametrize("cfg,split", [(2, 0), (2, 10 ** 9), (3, 8192), (3, 10 ** 9), (4, 10 ** 9),
+                                       (5, 10 ** 9)])
+def test_full_workload(cfg, split):
+    wl = make_workload(cfg)
+    split = min(split, wl.n_rows) if split else 0
+    st, _ = run(wl, split, with_part_seg=(cfg <= 3))
+    check_bookkeeping(wl, st, split, full_part_seg=(cfg <= 3))
+    g = wl.geom
+    kv = wl.kv()
+    keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    rows = boundary_sample(wl) if cfg <= 3 and split == 0 else _big_sample(wl, n_seg=3 if cfg >= 4 else 6)
+    compare_rows(wl, st, rows, None, kv=kv, keys=keys)
+
+
+@pytest.mark.parametrize("cfg", [2, 5])
+def test_full_workload_peaked(cfg):
+    """Far-from-uniform softmax at full size: unscaled queries and keys."""
+    wl = make_workload(cfg, "peaked")
+    split = wl.n_rows
+    st, _ = run(wl, split, with_part_seg=False)
+    g = wl.geom
+    kv = wl.kv()
+    keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    compare_rows(wl, st, _big_sample(wl, n_seg=3), None, kv=kv, keys=keys)
