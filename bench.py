@@ -50,6 +50,26 @@ def algorithmic_work(wl):
     return flop_attn, flop_oproj, head_rows
 
 
+def profiled_traffic():
+    """HBM-side bytes per attention launch from the committed rocprofv3 counter
+    summary, or None once the attention source differs from the profiled one."""
+    import hashlib
+    src = b"".join(open(os.path.join(ROOT, "paper_2609_07008_amd", "csrc", f), "rb").read()
+                   for f in ("attend.hip", "common.h"))
+    sha = hashlib.sha256(src).hexdigest()[:16]
+    path = os.path.join(ROOT, "profiles", "mla_online_step_256k.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        parts = line.strip().split(":")
+        if len(parts) == 2 and parts[0].startswith("attend_"):
+            fields[parts[0]] = parts[1].strip()
+    if fields.get("attend_source_sha256_16") != sha:
+        return None
+    return float(fields["attend_traffic_bytes_per_launch"])
+
+
 def cpu_baseline(wl, budget_s: float = 20.0):
     """The fp64 oracle as it stands, timed on a bounded sample of rows of the
     same workload: rows spread over the context (protected and unprotected)."""
@@ -100,6 +120,8 @@ def main():
                     help="chunking of each row's visible segments; -1 = one chunk per slot")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only: the step is measured on the "
@@ -111,6 +133,15 @@ def main():
     from paper_2609_07008_amd import device_inputs, step
 
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "copies": 3}), flush=True)
+        return
     wl = make_workload(args.workload)
     g = wl.geom
     split = wl.n_rows if args.split_keys < 0 else args.split_keys
@@ -175,7 +206,7 @@ def main():
                "wall_per_step": round(t_wall / args.steps * 1e3, 3), "upload_s": round(t_upload, 2)},
         "hbm_gbs": {"merge": round(merge_bytes / t_mrg / 1e9, 1), "oproj_add": round(oproj_bytes / t_opj / 1e9, 1)},
         "roofline": {"bound": "mfma", "achieved": round(att_tflops, 3), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4), "traffic": profiled_traffic(),
                      "kernel": "attend_kernel<512,64> (timed with the plan kernels of mla_online_attend)"},
     }
     if not args.no_cpu_baseline:
