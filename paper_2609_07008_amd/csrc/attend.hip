@@ -53,9 +53,15 @@ __device__ __forceinline__ int rotl3(int k) { return ((k << 1) | (k >> 2)) & 7; 
 // alias (it would wait for the prefetch of the next tile); the tile loop waits
 // for these loads explicitly (s_waitcnt vmcnt + barrier).
 __device__ __forceinline__ void dma16(const void* base, uint32_t voff, const unsigned char MLA_LDS* dst) {
-  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)dst);
+  const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(uintptr_t)dst);
+  // the base is wave-uniform; make that explicit so it is held in scalar registers.
+  // readfirstlane returns a signed int: zero-extend each half through uint32_t.
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(b >> 32));
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)b);
+  const uint64_t bs = ((uint64_t)hi << 32) | (uint64_t)lo;
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-               :: "v"(voff), "s"(base), "s"(m0) : "memory", "m0");
+               :: "v"(voff), "s"(bs), "s"(m0) : "memory", "m0");
 }
 
 __device__ __forceinline__ int wave_min_i(int v) {
@@ -278,6 +284,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   // accumulators, which stay in the matrix-core registers.
   const float sl2 = a.scale_log2;
   float m_init = -1e30f;
+  bool restarted = false;
   for (;;) {
 #pragma unroll
     for (int d = 0; d < C::OBH; ++d)
@@ -297,18 +304,17 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
     issue(L, cs, n_keys, 0);
 
     bool restart = false;
-    float mt = 0.f;
-    // one tile: prefetch the next into `nb`, wait for `cb`, score, exchange, accumulate.
-    // returns 0 = continue, 1 = chunk done, 2 = restart with a larger reference max
+    bool first_tile = !restarted;   // uniform over the workgroup
+    float mt = 0.f;   // this wave's row max of the current tile (log2 units)
+    // One tile.  Barrier A: the tile in `cb` has landed in LDS and every wave has
+    // finished the previous tile, so `nb` is free for the next prefetch.  Barrier C:
+    // softmax weights and restart votes are visible to the partner waves.
+    // Returns 0 = continue, 1 = chunk done, 2 = restart with a larger reference max.
     auto step = [&](const unsigned char MLA_LDS* cb, unsigned char MLA_LDS* nb) -> int {
-      const bool more = advance();
-      if (more) {
-        issue(nb, ns, n_keys, n_tile);
-        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(C::LOADS) : "memory");
-      } else {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __builtin_amdgcn_s_barrier();
+      const bool more = advance();
+      if (more) issue(nb, ns, n_keys, n_tile);
       const unsigned char MLA_LDS* buf = cb;
       // ---- S^T = K Q^T for this wave's 32 keys ----
       f32x16 sc;
@@ -325,12 +331,13 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
           }
           return *(const bf16x8 MLA_LDS*)(buf + abase[ks & 3] + (ks >> 2) * 1024);
         };
-        bf16x8 ka[2];
+        bf16x8 ka[3];
         ka[0] = kfrag(0);
+        if (C::KS > 1) ka[1] = kfrag(1);
 #pragma unroll
         for (int ks = 0; ks < C::KS; ++ks) {
-          if (ks + 1 < C::KS) ka[(ks + 1) & 1] = kfrag(ks + 1);
-          sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks & 1], qf[ks], sc, 0, 0, 0);
+          if (ks + 2 < C::KS) ka[(ks + 2) % 3] = kfrag(ks + 2);
+          sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks % 3], qf[ks], sc, 0, 0, 0);
         }
         // register e holds key kh*32 + half*4 + (e/4)*8 + e%4 of the tile, in log2 units
 #pragma unroll
@@ -346,15 +353,19 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
         float m = sc[0];
 #pragma unroll
         for (int e = 1; e < 16; ++e) m = fmaxf(m, sc[e]);
-        m = fmaxf(m, __shfl_xor(m, 32, 64));
-        if (half == 0) stat[wave][l32] = m;
+        mt = fmaxf(m, __shfl_xor(m, 32, 64));
       }
-      __builtin_amdgcn_s_barrier();
+      if (first_tile) {
+        // first tile of the item (workgroup-uniform): the pair fixes its common
+        // reference max
+        if (pair_active && half == 0) stat[wave][l32] = mt;
+        __builtin_amdgcn_s_barrier();
+        if (pair_active) m_run = fmaxf(stat[wave][l32], stat[wave ^ 1][l32]);
+        first_tile = false;
+      }
 
       bool up = false;
       if (pair_active) {
-        mt = fmaxf(stat[wave][l32], stat[wave ^ 1][l32]);
-        if (m_run < -1e29f) m_run = mt;                  // first tile: nothing accumulated yet
         up = __builtin_amdgcn_ballot_w64(mt > m_run + 64.f) != 0;
         // ---- softmax weights against the pair's common reference max ----
         float rsum = 0.f;
@@ -395,16 +406,16 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
           const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((MLA_LDS bf16x4*)(buf + off + C::KB8));
           return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         };
-        bf16x8 vt[2];
+        bf16x8 vt[3];
         vt[0] = vfrag(0);
+        if (NPV > 1) vt[1] = vfrag(1);
 #pragma unroll
         for (int st = 0; st < NPV; ++st) {
-          if (st + 1 < NPV) vt[(st + 1) & 1] = vfrag(st + 1);
+          if (st + 2 < NPV) vt[(st + 2) % 3] = vfrag(st + 2);
           const int d = st >> 2, j = (st >> 1) & 1, k2 = st & 1;
-          o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt[st & 1], pf[j][k2], o[d], 0, 0, 0);
+          o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt[st % 3], pf[j][k2], o[d], 0, 0, 0);
         }
       }
-      __builtin_amdgcn_s_barrier();
       if (!more) return 1;
       if (n_rank != c_rank) {   // the next tile opens a new segment
         c_rank = n_rank;
@@ -421,10 +432,14 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
       cur = C::TILE_BYTES - cur;
     }
     if (!restart) break;
-    // drain the prefetch in flight, then start over from the larger reference
+    // drain the prefetch in flight; the pair agrees on its tile max and starts
+    // over from the larger reference
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (pair_active && half == 0) stat[wave][l32] = mt;
     __builtin_amdgcn_s_barrier();
-    m_init = fmaxf(m_run, mt);
+    m_init = pair_active ? fmaxf(m_run, fmaxf(stat[wave][l32], stat[wave ^ 1][l32])) : 0.f;
+    restarted = true;
+    __builtin_amdgcn_s_barrier();
   }
 
   // ---- epilogue: combine the pair's row sums, store normalized partial and lse ----

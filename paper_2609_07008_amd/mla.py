@@ -40,10 +40,10 @@ class Segment(ctypes.Structure):
     _fields_ = [("kv_start", ctypes.c_int64), ("length", ctypes.c_int64), ("req_offset", ctypes.c_int64)]
 
 
-def _load():
-    if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_07008_amd.build`")
-    lib = ctypes.CDLL(LIB_PATH)
+def _load(path: str = LIB_PATH):
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run `python -m paper_2609_07008_amd.build`")
+    lib = ctypes.CDLL(path)
     P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     GP, SP = ctypes.POINTER(Geom), ctypes.POINTER(Segment)
     lib.mla_online_attend_query.argtypes = [GP, SP, I32, P, I32, I64, ctypes.POINTER(I64), ctypes.POINTER(I64),
