@@ -4,18 +4,23 @@
 //
 // Work item = up to 128 head-rows (query rows x heads) that share every key of
 // the single latent stream (the latent is never split per head, Sec. 2.1).
-// One 256-thread workgroup (4 waves x 32 head-rows) walks the item's visible
-// segments in request order; for each segment it rotates the RoPE part of its
-// queries by R(t - p_s) into the segment's canonical frame, then streams the
-// segment's 64-key latent tiles through LDS:
-//   S^T = K Q^T      (keys x head-rows, MFMA 32x32x16 bf16, K tile from LDS,
-//                     Q resident in registers)
-//   online softmax   (one head-row per lane pair, lazy rescaling)
-//   O^T += V^T P^T   (latent dims x head-rows, V = the same LDS tile read with
-//                     transposing LDS loads)
+// One 256-thread workgroup walks the item's visible segments in request order
+// and streams each segment's 64-key latent tiles through LDS once for all its
+// head-rows.  Each of the 4 waves owns 32 head-rows outright:
+//   relocation      rotate the RoPE part of its queries by R(t - p_s) into the
+//                   segment's canonical frame when a new segment starts
+//   S^T = K Q^T     64 keys x 32 head-rows (MFMA 32x32x16 bf16; K read from
+//                   LDS, the d_c + d_r query dims resident in registers)
+//   softmax         one head-row per lane pair, against a fixed reference max
+//   O^T += V^T P^T  d_c latent dims x 32 head-rows; V is the same LDS tile read
+//                   with transposing LDS loads, P^T is the S^T accumulator
+//                   rounded to bf16 in place (its lane layout is already the
+//                   MFMA operand layout once the keys are taken in the order
+//                   the V reads use)
 // and emits one normalized partial and one log-sum-exp per (slot, chunk).
-// Tiles are fetched with 16-byte direct-to-LDS loads, double-buffered, with the
-// 16-byte chunks of a key row XOR-swizzled so column reads hit distinct banks.
+// Tiles are fetched with 16-byte direct-to-LDS loads, double-buffered; the
+// 16-byte chunks of a key row are XOR-swizzled so row and column reads hit
+// distinct banks.
 #include "common.h"
 
 namespace mla {
@@ -37,12 +42,11 @@ struct Cfg {
   // banks.  KB8 = 128 mod 256 keeps 16-lane 16-byte reads conflict-free on 64 banks.
   static constexpr int KB8 = CG * 1024 + 128;
   static constexpr int TILE_BYTES = 8 * KB8;
-  static constexpr int LOADS = 2 * CG;       // direct loads per wave per tile (key-blocks 2w, 2w+1)
-  static constexpr int OB = DC / 32;         // 32-wide output blocks
-  static constexpr int OBH = OB / 2;         // output blocks owned by one wave
-  static constexpr int HR = 64;              // head-rows per work item
+  static constexpr int OB = DC / 32;         // 32-dim output blocks of O^T
+  static constexpr int PS = BK / 16;         // 16-key contraction steps of P.V per tile
   static_assert(DR == 16 || DR % 32 == 0, "d_rope must be 16 or a multiple of 32");
   static_assert(DC % 64 == 0, "d_latent must be a multiple of 64");
+  static_assert(kTileRows == 128, "one work item is 4 waves x 32 head-rows");
 };
 
 __device__ __forceinline__ int rotl3(int k) { return ((k << 1) | (k >> 2)) & 7; }
@@ -73,24 +77,55 @@ __device__ __forceinline__ int wave_min_i(int v) {
   return v;
 }
 
-// Work item = up to 64 head-rows as two blocks of 32.  Wave w serves head-row
-// block hb = w>>1 and half kh = w&1: it scores keys kh*32..kh*32+31 of each
-// 64-key tile and accumulates latent dims [kh*d_c/2, (kh+1)*d_c/2) of O for
-// all 64 keys, taking the other key half's softmax weights from its partner
-// wave w^1 through LDS.  Both waves of a pair see identical row maxima, so
-// they take identical rescaling decisions.
+// S^T accumulation on the matrix cores with the accumulators pinned to
+// architectural VGPRs: the O^T accumulators of the tile loop fill the whole
+// accumulation register file, so S^T is kept out of it.  Back-to-back
+// accumulation into the same registers needs no wait states; a vector ALU read
+// of the result does (s_acc_ready), and so does an MFMA read of a register that
+// a vector ALU op has just written (the leading s_nop of s_acc_first).
+__device__ __forceinline__ void s_acc_first(f32x16& s0, f32x16& s1, const bf16x8& k0, const bf16x8& k1,
+                                            const bf16x8& q) {
+  asm("s_nop 4\n\t"
+      "v_mfma_f32_32x32x16_bf16 %0, %2, %4, 0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %3, %4, 0"
+      : "=&v"(s0), "=&v"(s1)
+      : "v"(k0), "v"(k1), "v"(q));
+}
+__device__ __forceinline__ void s_acc(f32x16& s0, f32x16& s1, const bf16x8& k0, const bf16x8& k1,
+                                      const bf16x8& q) {
+  asm("v_mfma_f32_32x32x16_bf16 %0, %2, %4, %0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %3, %4, %1"
+      : "+v"(s0), "+v"(s1)
+      : "v"(k0), "v"(k1), "v"(q));
+}
+// 24 wait states: more than an XDL result needs before a vector ALU read
+__device__ __forceinline__ void s_acc_ready(f32x16& s0, f32x16& s1) {
+  asm("s_nop 15\n\ts_nop 7" : "+v"(s0), "+v"(s1));
+}
+
+// Tile barrier: this wave's direct-to-LDS loads and LDS accesses are complete,
+// then all waves meet.  One asm statement with a memory clobber, so the
+// compiler moves no LDS access across it.
+__device__ __forceinline__ void tile_barrier() {
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// value of lane l%32 and of lane l%32 + 32, in every lane (one permlane swap)
+__device__ __forceinline__ void lane_halves(float v, float& x, float& y) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  x = __uint_as_float(r[0]);
+  y = __uint_as_float(r[1]);
+}
+
 template <int DC, int DR>
 __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   using C = Cfg<DC, DR>;
   __shared__ __attribute__((aligned(16))) unsigned char lds[2 * C::TILE_BYTES];
-  __shared__ __attribute__((aligned(16))) bf16x8 pex[4][2][64];   // softmax weights for the partner
-  __shared__ float stat[4][32];                                    // row maxima / sums for the partner
-  __shared__ int restart_vote[4];
+  __shared__ unsigned restart_at;
 
   unsigned char MLA_LDS* L = (unsigned char MLA_LDS*)lds;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int hb = wave >> 1, kh = wave & 1;
   const int half = lane >> 5, l32 = lane & 31;
 
   // XCD-aware item order: blocks are dispatched round-robin over the 8 XCDs;
@@ -111,9 +146,9 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   const ChunkInfo chk = chunks[own.chunk_off + it.chunk];
 
   // ---- this lane's head-row ----
-  const int hr_local = hb * 32 + l32;
+  const int hr_local = wave * 32 + l32;
   const bool valid = hr_local < it.count;
-  const bool pair_active = hb * 32 < it.count;
+  const bool active = wave * 32 < it.count;   // wave-uniform: the wave has head-rows
   const int64_t hr = it.hr_begin + (valid ? hr_local : 0);
   int64_t row;
   const uint16_t* qsrc;
@@ -145,32 +180,33 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
     if (!valid) qf[ks] = bf16x8{};
   }
 
-  f32x16 o[C::OBH];
+  f32x16 o[C::OB];
   float m_run = -1e30f, l_run = 0.f;
 
   // ---- per-lane LDS address bases (everything else is an immediate offset) ----
-  // K as the A operand: key kh*32 + l32, chunk ks*2 + half
+  // K as the A operand: key kt*32 + l32 of the tile (kt adds 4 key-blocks), chunk
+  // 2*(ks&3) + half of chunk group ks>>2
   int abase[4];
 #pragma unroll
   for (int s4 = 0; s4 < 4; ++s4)
-    abase[s4] = (kh * 4 + (l32 >> 3)) * C::KB8 + (l32 & 7) * 128 + (((2 * s4 + half) ^ rotl3(l32 & 7)) * 16);
-  // V^T via transposing reads: in each 16-lane group q4 = lane/16, lane j = rr*4 + cb
-  // addresses key (q4>>1)*4 + rr of an 8-key block and latent dims (q4&1)*16 + cb*4 of
-  // a 32-dim block; lane j then receives dim j of those four keys.
+    abase[s4] = (l32 >> 3) * C::KB8 + (l32 & 7) * 128 + (((2 * s4 + half) ^ rotl3(l32 & 7)) * 16);
+  // V^T via transposing reads.  P.V step s2 contracts tile keys 16*s2 .. 16*s2+15 in
+  // the order the S^T accumulator holds them: lane half h takes keys 16*s2 + h*4 + 0..3
+  // (8-key block 2*s2) and 16*s2 + 8 + h*4 + 0..3 (block 2*s2 + 1).  In each 16-lane
+  // group q4 = lane/16, lane j = rr*4 + cb addresses key h*4 + rr of the block and
+  // latent dims (q4&1)*16 + cb*4 .. +3 of a 32-dim output block; lane j then receives
+  // dim (q4&1)*16 + j of those four keys.  Output block d covers chunk group d>>1 at
+  // chunk offset (d&1)*4; vb[d&1][s2>>1] is the base for block parity d&1 and key
+  // half s2>>1 of the tile, block d adds (d>>1)*1024 and step s2 adds (s2&1)*2*KB8.
   const int q4 = lane >> 4, rr = (lane >> 2) & 3, cb = lane & 3;
   const int vkey = (q4 >> 1) * 4 + rr;
-  // This wave owns output blocks x .. x+OBH-1 with x = kh*OBH; block x+d covers
-  // chunk group (x+d)>>1 at chunk offset ((x+d)&1)*4.  vb[d&1][j] is the base for
-  // local block parity d&1 and the key block of this wave (j = 0) or of its
-  // partner (j = 1); local block d adds (d>>1)*1024.
-  const int xb = kh * C::OBH;
   int vb[2][2];
 #pragma unroll
-  for (int dl = 0; dl < 2; ++dl)
+  for (int dp = 0; dp < 2; ++dp)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-      vb[dl][j] = vkey * 128 + (((((xb + dl) & 1) * 4 + (q4 & 1) * 2 + (cb >> 1)) ^ rotl3(vkey)) * 16) +
-                  (cb & 1) * 8 + (kh ^ j) * 4 * C::KB8 + ((xb + dl) >> 1) * 1024;
+    for (int kq = 0; kq < 2; ++kq)
+      vb[dp][kq] = vkey * 128 + (((dp * 4 + (q4 & 1) * 2 + (cb >> 1)) ^ rotl3(vkey)) * 16) + (cb & 1) * 8 +
+                   kq * 4 * C::KB8;
   // direct loads: lane l fills key l>>3 of an 8-key block, physical slot l&7
   const int lkey = lane >> 3;
   const int lchunk_full = (lane & 7) ^ rotl3(lkey);
@@ -276,22 +312,28 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
     return true;
   };
 
-  // The softmax reference max m_run is taken from the first tile.  A later tile
-  // whose max exceeds it by more than 2^64 (weights stay below 2^64: fp32 and
-  // bf16 hold them exactly enough) restarts the whole item from the larger
-  // reference; the decision is shared by the workgroup so every wave meets the
-  // same barriers.  The tile loop thus never applies vector ALU work to the O
-  // accumulators, which stay in the matrix-core registers.
+  // The softmax reference max m_run is the first tile's row max.  A later tile
+  // whose row max exceeds it by more than 2^64 (weights stay below 2^64, which
+  // fp32 sums and bf16 weights hold without loss) restarts the whole item from
+  // the largest max seen so far.  A wave that sees such a tile records its index
+  // (1-based) with an LDS atomic min in restart_at; after the barrier that opens
+  // tile t every wave tests restart_at <= t, which only votes cast before that
+  // barrier can satisfy, so all waves leave the tile loop at the same tile (the
+  // tiles computed in between are discarded with the rest).  The tile loop thus
+  // never applies vector ALU work to the O accumulators, which stay in the
+  // matrix-core accumulation registers.
   const float sl2 = a.scale_log2;
   float m_init = -1e30f;
   bool restarted = false;
+  if (tid == 0) restart_at = ~0u;   // ordered before any access by the first tile barrier
   for (;;) {
 #pragma unroll
-    for (int d = 0; d < C::OBH; ++d)
+    for (int d = 0; d < C::OB; ++d)
 #pragma unroll
       for (int e = 0; e < 16; ++e) o[d][e] = 0.f;
     m_run = m_init;
     l_run = 0.f;
+    float m_seen = m_init;
     c_rank = chk.first_rank;
     cs = segs[rank_seg[c_rank]];
     c_tile = 0;
@@ -305,159 +347,157 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
 
     bool restart = false;
     bool first_tile = !restarted;   // uniform over the workgroup
-    float mt = 0.f;   // this wave's row max of the current tile (log2 units)
-    // One tile.  Barrier A: the tile in `cb` has landed in LDS and every wave has
-    // finished the previous tile, so `nb` is free for the next prefetch.  Barrier C:
-    // softmax weights and restart votes are visible to the partner waves.
-    // Returns 0 = continue, 1 = chunk done, 2 = restart with a larger reference max.
-    auto step = [&](const unsigned char MLA_LDS* cb, unsigned char MLA_LDS* nb) -> int {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __builtin_amdgcn_s_barrier();
+    unsigned ti = 0;                 // tile index within the attempt (uniform)
+    int cur = 0;
+    for (;;) {
+      // The tile in buffer `cur` has landed (this wave's loads: vmcnt; the other
+      // waves' loads: the barrier), every wave has finished reading the other
+      // buffer, and the restart votes cast during the previous tile are visible.
+      tile_barrier();
+      if (*(volatile unsigned MLA_LDS*)&restart_at <= ti) {
+        restart = true;
+        break;
+      }
       const bool more = advance();
-      if (more) issue(nb, ns, n_keys, n_tile);
-      const unsigned char MLA_LDS* buf = cb;
-      // ---- S^T = K Q^T for this wave's 32 keys ----
-      f32x16 sc;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) sc[e] = 0.f;
-      if (pair_active) {
-        auto kfrag = [&](int ks) -> bf16x8 {
+      if (more) issue(L + (C::TILE_BYTES - cur), ns, n_keys, n_tile);
+      const unsigned char MLA_LDS* buf = L + cur;
+      if (active) {
+        // ---- S^T = K Q^T: keys 0..31 into s[0], keys 32..63 into s[1] ----
+        f32x16 s[2];
+        auto kfrag = [&](int kt, int ks) -> bf16x8 {
           if (DR == 16 && ks == C::CS) {
             // rope chunks 2*CS, 2*CS+1 sit in the partial (unswizzled) group: 8 bytes each
-            const int base0 = (kh * 4 + (l32 >> 3)) * C::KB8 + (l32 & 7) * 128 + C::CGF * 1024 + half * 8;
+            const int base0 = (kt * 4 + (l32 >> 3)) * C::KB8 + (l32 & 7) * 128 + C::CGF * 1024 + half * 8;
             const u32x2 x0 = *(const u32x2 MLA_LDS*)(buf + base0);
             const u32x2 y0 = *(const u32x2 MLA_LDS*)(buf + base0 + 16);
             return __builtin_bit_cast(bf16x8, u32x4{x0[0], x0[1], y0[0], y0[1]});
           }
-          return *(const bf16x8 MLA_LDS*)(buf + abase[ks & 3] + (ks >> 2) * 1024);
+          return *(const bf16x8 MLA_LDS*)(buf + abase[ks & 3] + (ks >> 2) * 1024 + kt * 4 * C::KB8);
         };
-        bf16x8 ka[3];
-        ka[0] = kfrag(0);
-        if (C::KS > 1) ka[1] = kfrag(1);
+        // K fragments are read two steps ahead of their MFMAs; the scheduling
+        // barriers keep the compiler from sinking the reads next to their use
+        bf16x8 ka[3][2];
+        ka[0][0] = kfrag(0, 0);
+        ka[0][1] = kfrag(1, 0);
+        ka[1][0] = kfrag(0, 1);
+        ka[1][1] = kfrag(1, 1);
 #pragma unroll
         for (int ks = 0; ks < C::KS; ++ks) {
-          if (ks + 2 < C::KS) ka[(ks + 2) % 3] = kfrag(ks + 2);
-          sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks % 3], qf[ks], sc, 0, 0, 0);
-        }
-        // register e holds key kh*32 + half*4 + (e/4)*8 + e%4 of the tile, in log2 units
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sc[e] *= sl2;
-        const int tk0 = (int)(c_tile * C::BK) + kh * 32;
-        if (tk0 + 31 > wave_lim) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int key = tk0 + half * 4 + (e >> 2) * 8 + (e & 3);
-            if (key > lim) sc[e] = -INFINITY;
+          if (ks + 2 < C::KS) {
+            ka[(ks + 2) % 3][0] = kfrag(0, ks + 2);
+            ka[(ks + 2) % 3][1] = kfrag(1, ks + 2);
           }
+          __builtin_amdgcn_sched_barrier(0);
+          if (ks == 0)
+            s_acc_first(s[0], s[1], ka[0][0], ka[0][1], qf[0]);
+          else
+            s_acc(s[0], s[1], ka[ks % 3][0], ka[ks % 3][1], qf[ks]);
+          __builtin_amdgcn_sched_barrier(0);
         }
-        float m = sc[0];
-#pragma unroll
-        for (int e = 1; e < 16; ++e) m = fmaxf(m, sc[e]);
-        mt = fmaxf(m, __shfl_xor(m, 32, 64));
-      }
-      if (first_tile) {
-        // first tile of the item (workgroup-uniform): the pair fixes its common
-        // reference max
-        if (pair_active && half == 0) stat[wave][l32] = mt;
-        __builtin_amdgcn_s_barrier();
-        if (pair_active) m_run = fmaxf(stat[wave][l32], stat[wave ^ 1][l32]);
-        first_tile = false;
-      }
-
-      bool up = false;
-      if (pair_active) {
-        up = __builtin_amdgcn_ballot_w64(mt > m_run + 64.f) != 0;
-        // ---- softmax weights against the pair's common reference max ----
-        float rsum = 0.f;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          sc[e] = __builtin_amdgcn_exp2f(sc[e] - m_run);
-          rsum += sc[e];
-        }
-        l_run += rsum + __shfl_xor(rsum, 32, 64);          // this wave's 32 keys only
-        bf16x8 pown[2];
-#pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-          for (int i = 0; i < 8; ++i) pown[k2][i] = (__bf16)sc[k2 * 8 + i];
-        pex[wave][0][lane] = pown[0];
-        pex[wave][1][lane] = pown[1];
-      }
-      if (lane == 0) restart_vote[wave] = up ? 1 : 0;
-      __builtin_amdgcn_s_barrier();
-      // a row whose tile max passed the reference by 2^64: the whole workgroup
-      // discards this tile and restarts (l_run is reset with the restart)
-      restart = (restart_vote[0] | restart_vote[1] | restart_vote[2] | restart_vote[3]) != 0;
-      if (restart) return 2;
-
-      if (pair_active) {
-        // ---- O^T[dims of half kh] += V^T P^T over all 64 keys ----
-        // contraction order: this wave's key block, then the partner's
-        bf16x8 pf[2][2];   // [own, partner][k step]
-        pf[0][0] = pex[wave][0][lane];
-        pf[0][1] = pex[wave][1][lane];
-        pf[1][0] = pex[wave ^ 1][0][lane];
-        pf[1][1] = pex[wave ^ 1][1][lane];
-        constexpr int NPV = C::OBH * 4;
+        // the first V^T fragments of P.V do not depend on the softmax: read them now
+        constexpr int NPV = C::PS * C::OB;
+        constexpr int VD = 3;   // V^T fragments in flight ahead of their MFMA
         auto vfrag = [&](int st) -> bf16x8 {
-          const int d = st >> 2, j = (st >> 1) & 1, k2 = st & 1;
-          const int off = vb[d & 1][j] + (d >> 1) * 1024 + k2 * 2 * C::KB8;
+          const int s2 = st / C::OB, d = st % C::OB;
+          const int off = vb[d & 1][s2 >> 1] + (d >> 1) * 1024 + (s2 & 1) * 2 * C::KB8;
           const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((MLA_LDS bf16x4*)(buf + off));
           const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((MLA_LDS bf16x4*)(buf + off + C::KB8));
           return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         };
-        bf16x8 vt[3];
-        vt[0] = vfrag(0);
-        if (NPV > 1) vt[1] = vfrag(1);
+        bf16x8 vt[VD + 1];
+#pragma unroll
+        for (int j = 0; j < VD; ++j) vt[j] = vfrag(j);
+        __builtin_amdgcn_sched_barrier(0);
+        s_acc_ready(s[0], s[1]);
+        // register e of s[kt] holds tile key kt*32 + half*4 + (e/4)*8 + e%4 (raw Q.K)
+        const int tk0 = (int)(c_tile * C::BK);
+        if (tk0 + C::BK - 1 > wave_lim) {
+          // visible iff (e/4)*8 + e%4 (+32 for s[1]) <= lim - tk0 - half*4; the lane
+          // half is recomputed from the lane id rather than kept live across the loop
+          const int rel = lim - tk0 - ((int)(__lane_id() >> 5) << 2);
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int key = (e >> 2) * 8 + (e & 3);
+            if (key > rel) s[0][e] = -INFINITY;
+            if (key + 32 > rel) s[1][e] = -INFINITY;
+          }
+        }
+        float m = fmaxf(s[0][0], s[1][0]);
+#pragma unroll
+        for (int e = 1; e < 16; ++e) m = fmaxf(m, fmaxf(s[0][e], s[1][e]));
+        float mx, my;
+        lane_halves(m, mx, my);
+        const float mt = fmaxf(mx, my) * sl2;   // row max of the tile, log2 units (sl2 > 0)
+        if (first_tile) m_run = mt;
+        m_seen = fmaxf(m_seen, mt);
+        if (__builtin_amdgcn_ballot_w64(mt > m_run + 64.f) != 0 && lane == 0) atomicMin(&restart_at, ti + 1);
+        // ---- softmax weights 2^(s*scale*log2e - m_run), rounded to bf16 in place:
+        // pf[s2] is the B operand (P^T) of P.V step s2 ----
+        bf16x8 pf[C::PS];
+        float rsum = 0.f;
+        const float nm = -m_run;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][e], sl2, nm));
+            rsum += p;
+            pf[kt * 2 + (e >> 3)][e & 7] = (__bf16)p;
+          }
+        l_run += rsum;   // this lane's keys only; the two halves are combined at the end
+
+        // ---- O^T += V^T P^T over the 64 keys: 16-key steps outer, output blocks inner ----
 #pragma unroll
         for (int st = 0; st < NPV; ++st) {
-          if (st + 2 < NPV) vt[(st + 2) % 3] = vfrag(st + 2);
-          const int d = st >> 2, j = (st >> 1) & 1, k2 = st & 1;
-          o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt[st % 3], pf[j][k2], o[d], 0, 0, 0);
+          if (st + VD < NPV) vt[(st + VD) % (VD + 1)] = vfrag(st + VD);
+          __builtin_amdgcn_sched_barrier(0);
+          const int s2 = st / C::OB, d = st % C::OB;
+          o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt[st % (VD + 1)], pf[s2], o[d], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
-      if (!more) return 1;
+      first_tile = false;
+      ++ti;
+      if (!more) break;
       if (n_rank != c_rank) {   // the next tile opens a new segment
         c_rank = n_rank;
         cs = ns;
         relocate(cs);
       }
       c_tile = n_tile;
-      return 0;
-    };
-    int cur = 0;
-    for (;;) {
-      const int r = step(L + cur, L + (C::TILE_BYTES - cur));
-      if (r != 0) break;
       cur = C::TILE_BYTES - cur;
     }
-    if (!restart) break;
-    // drain the prefetch in flight; the pair agrees on its tile max and starts
-    // over from the larger reference
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    if (pair_active && half == 0) stat[wave][l32] = mt;
-    __builtin_amdgcn_s_barrier();
-    m_init = pair_active ? fmaxf(m_run, fmaxf(stat[wave][l32], stat[wave ^ 1][l32])) : 0.f;
+    if (!restart) {
+      // votes cast during the last tile
+      tile_barrier();
+      restart = *(volatile unsigned MLA_LDS*)&restart_at != ~0u;
+      if (!restart) break;
+    }
+    // every wave has seen the vote: drain the loads in flight, clear the vote
+    // (ordered before the next votes by the next attempt's first tile barrier)
+    // and start over from the largest row max seen
+    tile_barrier();
+    if (tid == 0) restart_at = ~0u;
+    m_init = m_seen;
     restarted = true;
-    __builtin_amdgcn_s_barrier();
   }
 
-  // ---- epilogue: combine the pair's row sums, store normalized partial and lse ----
-  if (pair_active && half == 0) stat[wave][l32] = l_run;
-  __syncthreads();
+  // ---- epilogue: combine the two lane halves' row sums, store normalized partial and lse ----
+  float lx, ly;
+  lane_halves(l_run, lx, ly);
   if (!valid) return;
-  const float l_tot = l_run + stat[wave ^ 1][l32];
+  const float l_tot = lx + ly;
   const int64_t pidx = a.part_ptr[slot] + it.chunk;
   const float inv = 1.f / l_tot;
-  float* dst = a.part_o + pidx * DC + kh * (DC / 2);
+  float* dst = a.part_o + pidx * DC;
 #pragma unroll
-  for (int d = 0; d < C::OBH; ++d)
+  for (int d = 0; d < C::OB; ++d)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       f32x4 v = {o[d][4 * i] * inv, o[d][4 * i + 1] * inv, o[d][4 * i + 2] * inv, o[d][4 * i + 3] * inv};
       *(f32x4*)(dst + d * 32 + half * 4 + 8 * i) = v;
     }
-  if (kh == 0 && half == 0) a.part_lse[pidx] = (m_run + __log2f(l_tot)) * 0.6931471805599453f;
+  if (half == 0) a.part_lse[pidx] = (m_run + __log2f(l_tot)) * 0.6931471805599453f;
 }
 
 // ----------------------------------------------------------------------------

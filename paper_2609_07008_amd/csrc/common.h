@@ -18,7 +18,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #define MLA_LDS __attribute__((address_space(3)))
 
 constexpr int kMaxRopePairs = 32;   // d_rope <= 64
-constexpr int kTileRows = 64;       // head-rows per attention work item (2 blocks of 32)
+constexpr int kTileRows = 128;      // head-rows per attention work item (4 waves x 32)
 constexpr int kMaxGroups = 128;
 
 // ----------------------------------------------------------------------------
