@@ -70,9 +70,52 @@ def profiled_traffic():
     return float(fields["attend_traffic_bytes_per_launch"])
 
 
+def stratified_rows(wl, seed: int = 7):
+    """Row sample for the oracle, interleaving the row kinds of the workload: the
+    first and last row of every segment and the rows on both sides of each
+    segment boundary (in request order), protected document rows, unprotected
+    document rows and query rows (the query block is the last segment).  Seeded;
+    the order alternates kinds so a time-bounded prefix still covers all of them."""
+    rng = np.random.default_rng(seed)
+    segs = np.asarray(wl.segs, dtype=np.int64)
+    n = wl.n_rows
+    prot = np.asarray(wl.prot_rows, dtype=np.int64)
+    q0 = int(segs[np.argmax(segs[:, 2]), 0])          # first storage row of the query block
+    is_prot = np.zeros(n, dtype=bool)
+    is_prot[prot] = True
+    edges = []
+    for ks, ln, _ in segs[np.argsort(segs[:, 2])]:
+        edges += [int(ks), int(ks + ln - 1)]
+    doc = np.arange(q0)
+    kinds = [rng.permutation(np.unique(edges)),
+             rng.permutation(prot[prot < q0]),
+             rng.permutation(doc[~is_prot[:q0]]),
+             np.concatenate([[q0, n - 1], rng.permutation(np.arange(q0 + 1, n - 1))])]
+    out, seen, i = [], set(), 0
+    while any(i < len(k) for k in kinds):
+        for k in kinds:
+            if i < len(k) and int(k[i]) not in seen:
+                seen.add(int(k[i]))
+                out.append(int(k[i]))
+        i += 1
+        if len(out) >= 1024:
+            break
+    return out
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(wl, budget_s: float = 20.0):
-    """The fp64 oracle as it stands, timed on a bounded sample of rows of the
-    same workload: rows spread over the context (protected and unprotected)."""
+    """The fp64 oracle as it stands, timed on a bounded prefix of a stratified row
+    sample of the same workload (all online heads of each row, unfactorized)."""
     import oracle as O
     try:
         from threadpoolctl import threadpool_info
@@ -80,22 +123,19 @@ def cpu_baseline(wl, budget_s: float = 20.0):
     except Exception:  # noqa: BLE001
         cores = len(os.sched_getaffinity(0))
     g = wl.geom
-    rng = np.random.default_rng(7)
     t0 = time.perf_counter()
     kv = wl.kv()
     keys = O.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
     w_o = wl.w_o()
     setup = time.perf_counter() - t0
     prot = set(np.asarray(wl.prot_rows).tolist())
-    cand = rng.permutation(wl.n_rows)
     pos = np.empty(wl.n_rows, dtype=np.int64)
     for ks, ln, ro in wl.segs:
         pos[ks:ks + ln] = ro + np.arange(ln)
     per_key = 2.0 * g.d_qk + 2.0 * g.d_latent
     done_rows, flops, elapsed = 0, 0.0, 0.0
     t_start = time.perf_counter()
-    for r in cand:
-        r = int(r)
+    for r in stratified_rows(wl):
         zr = wl.z_off(rows=[r])
         O.reference_rows(wl, [r], z_off={r: zr[0]}, kv=kv, keys=keys, w_o=w_o)
         heads = g.n_groups + (g.n_local if r in prot else 0)
@@ -105,9 +145,50 @@ def cpu_baseline(wl, budget_s: float = 20.0):
         if elapsed > budget_s:
             break
     return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "rows_per_s": done_rows / elapsed,
-            "sample": f"{done_rows} random rows of the same workload (fp64, all online heads of each row, "
-                      f"unfactorized), {elapsed:.1f} s after {setup:.1f} s of key setup"}
+            "rows_per_s": done_rows / elapsed, "cpu": cpu_model(),
+            "sample": f"first {done_rows} rows of a stratified sample of the same workload (segment edges, "
+                      f"protected / unprotected document rows, query rows; fp64, all online heads of each "
+                      f"row, unfactorized), {elapsed:.1f} s after {setup:.1f} s of key setup"}
+
+
+def merge_per_segment(wl, torch, stream, reps: int = 3):
+    """Standalone mla_segment_merge on per-segment partials of the workload's query
+    rows: every query-row slot (Global and Local heads) holds one partial per
+    visible segment.  Partials are synthetic (the merge reads them, nothing else
+    depends on their values); returns merged slot rows/s and achieved GB/s."""
+    from paper_2609_07008_amd import mla
+    g = wl.geom
+    segs = np.asarray(wl.segs, dtype=np.int64)
+    q0 = int(segs[np.argmax(segs[:, 2]), 0])
+    n_q = wl.n_rows - q0
+    n_slots = n_q * g.n_heads
+    per_slot = int(segs.shape[0])                      # query rows see every segment
+    n_parts = n_slots * per_slot
+    dev = "cuda"
+    part_o = torch.empty((n_parts, g.d_latent), dtype=torch.float32, device=dev).normal_()
+    part_lse = torch.empty(n_parts, dtype=torch.float32, device=dev).normal_()
+    part_ptr = torch.arange(0, n_parts + 1, per_slot, dtype=torch.int64, device=dev)
+    out_o = torch.empty((n_slots, g.d_latent), dtype=torch.bfloat16, device=dev)
+    out_lse = torch.empty(n_slots, dtype=torch.float32, device=dev)
+    args = (n_slots, g.d_latent, part_o, part_lse, part_ptr, mla.MLA_BF16, out_o, out_lse)
+    mla.segment_merge(*args, stream=stream)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        mla.segment_merge(*args, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) / 1e3)
+    t = float(np.median(ts))
+    nbytes = n_parts * (4 * g.d_latent + 4) + n_slots * (2 * g.d_latent + 4) + (n_slots + 1) * 8
+    del part_o, part_lse, part_ptr, out_o, out_lse
+    torch.cuda.empty_cache()
+    return {"partials": n_parts, "slots": n_slots, "query_rows": n_q, "partials_per_slot": per_slot,
+            "ms": round(t * 1e3, 3), "slot_rows_per_s": round(n_slots / t, 1),
+            "query_rows_per_s": round(n_q / t, 1), "gb_s": round(nbytes / t / 1e9, 1),
+            "pct_hbm_peak": round(100 * nbytes / t / 1e9 / PEAK_HBM_GBS, 1)}
 
 
 def main():
@@ -119,6 +200,8 @@ def main():
     ap.add_argument("--split-keys", type=int, default=-1,
                     help="chunking of each row's visible segments; -1 = one chunk per slot")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-merge-per-segment", action="store_true",
+                    help="skip the standalone merge of per-segment partials of the query rows")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (reference for HBM byte counters)")
@@ -171,10 +254,10 @@ def main():
         e[3].record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
-    t_att = np.mean([e[0].elapsed_time(e[1]) for e in ev]) / 1e3
-    t_mrg = np.mean([e[1].elapsed_time(e[2]) for e in ev]) / 1e3
-    t_opj = np.mean([e[2].elapsed_time(e[3]) for e in ev]) / 1e3
-    t_step = np.mean([e[0].elapsed_time(e[3]) for e in ev]) / 1e3
+    t_att = np.median([e[0].elapsed_time(e[1]) for e in ev]) / 1e3
+    t_mrg = np.median([e[1].elapsed_time(e[2]) for e in ev]) / 1e3
+    t_opj = np.median([e[2].elapsed_time(e[3]) for e in ev]) / 1e3
+    t_step = np.median([e[0].elapsed_time(e[3]) for e in ev]) / 1e3
 
     value = (flop_attn + flop_oproj) / t_step / 1e12
     att_tflops = flop_attn / t_att / 1e12
@@ -209,6 +292,10 @@ def main():
                      "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4), "traffic": profiled_traffic(),
                      "kernel": "attend_kernel<512,64> (timed with the plan kernels of mla_online_attend)"},
     }
+    if not args.no_merge_per_segment:
+        del st
+        torch.cuda.empty_cache()
+        out["merge_per_segment"] = merge_per_segment(wl, torch, stream)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
     print(json.dumps(out), flush=True)
