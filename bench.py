@@ -191,6 +191,60 @@ def merge_per_segment(wl, torch, stream, reps: int = 3):
             "pct_hbm_peak": round(100 * nbytes / t / 1e9 / PEAK_HBM_GBS, 1)}
 
 
+def offline_producer(wl, torch, stream, reps: int = 2, seed: int = 70080):
+    """mla_offline_produce (the MLA-Off native producer) on the workload's geometry
+    and segment table: the Local-head artifact of every row.  Inputs are drawn on
+    the device (torch.Generator seeded with `seed`; latent and queries ~ N(0, 1/dim),
+    W_o std 0.02, as the workload's recipe) because the all-row Local-head queries
+    are too large to draw on the host within the benchmark's time."""
+    from paper_2609_07008_amd import mla
+    g = wl.geom
+    n = wl.n_rows
+    hl = g.heads_per_group - 1
+    if hl < 1:
+        return None
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(seed)
+
+    def draw(shape, std):
+        x = torch.empty(shape, dtype=torch.float32, device="cuda").normal_(0.0, 1.0, generator=gen)
+        return (x * std).to(torch.bfloat16)
+
+    kv = torch.cat([draw((n, g.d_latent), g.d_latent ** -0.5), draw((n, g.d_rope), g.d_rope ** -0.5)], 1)
+    q = torch.empty((n, g.n_groups, hl, g.d_qk), dtype=torch.bfloat16, device="cuda")
+    for c0 in range(0, n, 16384):   # chunked draw keeps the float32 staging small
+        c1 = min(n, c0 + 16384)
+        q[c0:c1, :, :, :g.d_latent] = draw((c1 - c0, g.n_groups, hl, g.d_latent), g.d_latent ** -0.5)
+        q[c0:c1, :, :, g.d_latent:] = draw((c1 - c0, g.n_groups, hl, g.d_rope), g.d_rope ** -0.5)
+    rows_w = (g.n_heads // g.n_proj_groups) * g.d_latent
+    w_o = draw((g.n_proj_groups, rows_w, g.d_model // g.n_proj_groups), 0.02)
+    z = torch.empty((n, g.d_model), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(mla.offline_produce_query(g, wl.segs), dtype=torch.uint8, device="cuda")
+    args = (g, wl.segs, kv, q, wl.glob_head, w_o, mla.MLA_BF16, z, ws)
+    mla.offline_produce(*args, stream=stream)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        mla.offline_produce(*args, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) / 1e3)
+    t = float(np.median(ts))
+    # algorithmic work: each row's Local heads attend to u+1 keys of their own segment
+    keys = float(sum(int(ln) * (int(ln) + 1) // 2 for _, ln, _ in np.asarray(wl.segs)))
+    flop_attn = keys * g.n_groups * hl * (2.0 * g.d_qk + 2.0 * g.d_latent)
+    flop_proj = n * g.n_groups * hl * 2.0 * g.d_latent * g.d_model / g.n_proj_groups
+    del kv, q, w_o, z, ws
+    torch.cuda.empty_cache()
+    return {"ms": round(t * 1e3, 3), "rows_per_s": round(n / t, 1), "flop": flop_attn + flop_proj,
+            "tflops": round((flop_attn + flop_proj) / t / 1e12, 3),
+            "pct_bf16_peak": round(100 * (flop_attn + flop_proj) / t / 1e12 / PEAK_BF16_TFLOPS, 2),
+            "local_head_rows": n * g.n_groups * hl, "out": "bf16 [rows, d_model]",
+            "inputs": f"device-drawn, torch.Generator seed {seed}"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,6 +256,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-merge-per-segment", action="store_true",
                     help="skip the standalone merge of per-segment partials of the query rows")
+    ap.add_argument("--no-offline-producer", action="store_true",
+                    help="skip the MLA-Off producer measurement on the same geometry")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (reference for HBM byte counters)")
@@ -292,10 +348,12 @@ def main():
                      "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4), "traffic": profiled_traffic(),
                      "kernel": "attend_kernel<512,64> (timed with the plan kernels of mla_online_attend)"},
     }
+    del st, dev
+    torch.cuda.empty_cache()
     if not args.no_merge_per_segment:
-        del st
-        torch.cuda.empty_cache()
         out["merge_per_segment"] = merge_per_segment(wl, torch, stream)
+    if not args.no_offline_producer:
+        out["offline_producer"] = offline_producer(wl, torch, stream)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -193,6 +193,41 @@ mla_status mla_sliced_oproj_add(const mla_geom* geom, int64_t n_rows, const void
                                 const int32_t* prot_rows, int32_t n_prot, const void* w_o,
                                 const void* z_off, float* z, void* stream);
 
+/* ----------------------------------------------------------------------------
+ * mla_offline_produce -- the MLA-Off native producer (Alg. 1, NativeProducer;
+ * eq:offonline): the Local-head artifact of every row of every segment,
+ *   z_off[r] = sum_{h Local} W_block(h)^T O_h^can[r],
+ * where O_h^can[r] attends only to the keys of r's own segment with canonical
+ * offsets u' <= u_r, the query's RoPE part rotated to its canonical position
+ * u_r (the segment evaluated alone, its first row at position 0).  The result is
+ * what mla_sliced_oproj_add reads as z_off.  Every segment of the table is
+ * produced, the query block included (a caller that only needs document rows
+ * ignores the others).
+ *
+ *   geom           as for mla_sliced_oproj_add (n_proj_groups, d_model used).
+ *   segs, n_segs   segment table as for mla_online_attend (host).
+ *   kv             [N, D] bf16 device: packed latent || canonical RoPE key.
+ *   q_loc          [N, G, hpg-1, D] bf16 device: the Local-head queries of every
+ *                  row (Local heads of group g in ascending head index, the
+ *                  Global head glob_head[g] skipped); RoPE part unrotated.
+ *   glob_head      [G] host: in-group index of each group's Global head.
+ *   w_o            as for mla_sliced_oproj_add.
+ *   out_dtype      MLA_BF16 or MLA_F32: element type of z_off.
+ *   z_off          [N, d_model] device, written (every element).
+ *   workspace      device, 256-byte aligned, at least the size returned by
+ *                  mla_offline_produce_query: plan, bf16 head outputs
+ *                  [N, G, hpg-1, d_c].  Overwritten.
+ * With hpg == 1 (no Local heads) z_off is written with zeros.  Errors as for
+ * mla_online_attend.
+ * ------------------------------------------------------------------------- */
+mla_status mla_offline_produce_query(const mla_geom* geom, const mla_segment* segs, int32_t n_segs,
+                                     size_t* ws_bytes);
+
+mla_status mla_offline_produce(const mla_geom* geom, const mla_segment* segs, int32_t n_segs,
+                               const void* kv, const void* q_loc, const int32_t* glob_head,
+                               const void* w_o, int32_t out_dtype, void* z_off, void* workspace,
+                               size_t ws_bytes, void* stream);
+
 /* Static description of a status code. */
 const char* mla_status_str(mla_status s);
 

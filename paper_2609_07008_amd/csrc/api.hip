@@ -115,8 +115,10 @@ struct Plan {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// offline: the producer's plan (Alg. 1) -- every segment sees only itself, and
+// only Local heads run (every row is listed in prot, no Global slots exist).
 mla_status build_plan(const mla_geom* g, const mla_segment* segs, int32_t n_segs, const int32_t* prot,
-                      int32_t n_prot, int64_t split_keys, bool want_blob, Plan* out) {
+                      int32_t n_prot, int64_t split_keys, bool want_blob, Plan* out, bool offline = false) {
   mla_status st = check_geom(g, false);
   if (st != MLA_OK) return st;
   int64_t N = 0;
@@ -146,6 +148,11 @@ mla_status build_plan(const mla_geom* g, const mla_segment* segs, int32_t n_segs
     info[s].req_offset = segs[s].req_offset;
     info[s].rank = rank_of[s];
     info[s].chunk_off = (int32_t)chunks.size();
+    if (offline) {
+      chunks.push_back({rank_of[s], rank_of[s]});
+      info[s].n_chunks = 1;
+      continue;
+    }
     int32_t first = 0;
     int64_t keys = 0;
     for (int32_t r = 0; r <= rank_of[s]; ++r) {
@@ -166,7 +173,7 @@ mla_status build_plan(const mla_geom* g, const mla_segment* segs, int32_t n_segs
   int64_t cum = 0;
   for (int32_t i : storage) {
     info[i].cum_global = cum;
-    cum += (int64_t)G * info[i].length * info[i].n_chunks;
+    if (!offline) cum += (int64_t)G * info[i].length * info[i].n_chunks;
   }
   const int64_t global_parts = cum;
   std::vector<int32_t> prot_seg(n_prot);
@@ -179,7 +186,7 @@ mla_status build_plan(const mla_geom* g, const mla_segment* segs, int32_t n_segs
       cum_local[a + 1] = cum_local[a] + Lh * info[storage[si]].n_chunks;
     }
   }
-  const int64_t n_slots = N * G + (int64_t)n_prot * Lh;
+  const int64_t n_slots = (offline ? 0 : N * G) + (int64_t)n_prot * Lh;
   const int64_t n_parts = global_parts + cum_local[n_prot];
 
   // work items: per segment, its rows' head-rows in runs of 64, times its chunks
@@ -213,9 +220,10 @@ mla_status build_plan(const mla_geom* g, const mla_segment* segs, int32_t n_segs
       }
     }
   };
-  for (int32_t s = 0; s < n_segs; ++s)
-    add_items(0, s, segs[s].kv_start * G, (segs[s].kv_start + segs[s].length) * G,
-              [&](int64_t hr) { return hr / G; });
+  if (!offline)
+    for (int32_t s = 0; s < n_segs; ++s)
+      add_items(0, s, segs[s].kv_start * G, (segs[s].kv_start + segs[s].length) * G,
+                [&](int64_t hr) { return hr / G; });
   if (Lh > 0) {
     int32_t a = 0;
     while (a < n_prot) {
@@ -405,6 +413,8 @@ mla_status mla_online_attend(const mla_geom* geom, const mla_segment* segs, int3
   a.d_latent = geom->d_latent;
   a.d_rope = geom->d_rope;
   a.scale_log2 = geom->softmax_scale * 1.4426950408889634f;
+  a.local_slot_base = p.hdr.n_rows * geom->n_groups;
+  a.out_bf16 = nullptr;
   a.hdr = p.hdr;
   hipError_t e = mla::launch_plan(a, s);
   if (e != hipSuccess) return hip_fail(e, "plan kernels");
@@ -464,8 +474,123 @@ mla_status mla_sliced_oproj_add(const mla_geom* geom, int64_t n_rows, const void
   a.d_model = geom->d_model;
   a.n_pg = geom->n_proj_groups;
   for (int g = 0; g < geom->n_groups; ++g) a.glob_head[g] = glob_head[g];
-  hipError_t e = mla::launch_oproj(a, reinterpret_cast<hipStream_t>(stream));
+  a.z_bf16 = 0;
+  hipError_t e = mla::launch_oproj(a, 3, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "o-proj kernels");
+  return MLA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// MLA-Off producer (Alg. 1 NativeProducer)
+// ---------------------------------------------------------------------------
+namespace {
+
+struct OfflineLayout {
+  Plan plan;
+  std::vector<int32_t> rows;   // identity row list: every row computes its Local heads
+  size_t off_o = 0;            // bf16 head outputs [N, G, hpg-1, d_c]
+  size_t total = 0;
+};
+
+mla_status offline_layout(const mla_geom* geom, const mla_segment* segs, int32_t n_segs, bool want_blob,
+                          OfflineLayout* L) {
+  mla_status st = check_geom(geom, true);
+  if (st != MLA_OK) return st;
+  int64_t N = 0;
+  if ((st = check_segments(segs, n_segs, &N)) != MLA_OK) return st;
+  L->rows.resize((size_t)N);
+  std::iota(L->rows.begin(), L->rows.end(), 0);
+  if ((st = build_plan(geom, segs, n_segs, L->rows.data(), (int32_t)N, 0, want_blob, &L->plan, true)) != MLA_OK)
+    return st;
+  const int hpg = geom->n_heads / geom->n_groups;
+  const size_t o_bytes = (size_t)N * geom->n_groups * (hpg - 1) * geom->d_latent * 2;
+  L->off_o = align_up((size_t)L->plan.hdr.total_bytes, 256);
+  L->total = L->off_o + align_up(o_bytes, 256);
+  return MLA_OK;
+}
+
+}  // namespace
+
+mla_status mla_offline_produce_query(const mla_geom* geom, const mla_segment* segs, int32_t n_segs,
+                                     size_t* ws_bytes) {
+  g_detail.clear();
+  if (ws_bytes == nullptr) return fail(MLA_ERR_NULL, "ws_bytes is NULL");
+  OfflineLayout L;
+  const mla_status st = offline_layout(geom, segs, n_segs, false, &L);
+  if (st != MLA_OK) return st;
+  *ws_bytes = L.total;
+  return MLA_OK;
+}
+
+mla_status mla_offline_produce(const mla_geom* geom, const mla_segment* segs, int32_t n_segs, const void* kv,
+                               const void* q_loc, const int32_t* glob_head, const void* w_o, int32_t out_dtype,
+                               void* z_off, void* workspace, size_t ws_bytes, void* stream) {
+  g_detail.clear();
+  OfflineLayout L;
+  mla_status st = offline_layout(geom, segs, n_segs, true, &L);
+  if (st != MLA_OK) return st;
+  const int hpg = geom->n_heads / geom->n_groups;
+  const int64_t N = L.plan.hdr.n_rows;
+  if (out_dtype != MLA_BF16 && out_dtype != MLA_F32) return fail(MLA_ERR_SHAPE, "out_dtype %d", out_dtype);
+  if (glob_head == nullptr) return fail(MLA_ERR_NULL, "glob_head is NULL");
+  for (int g = 0; g < geom->n_groups; ++g)
+    if (glob_head[g] < 0 || glob_head[g] >= hpg)
+      return fail(MLA_ERR_SHAPE, "glob_head[%d] = %d outside [0, %d)", g, glob_head[g], hpg);
+  if (z_off == nullptr || workspace == nullptr) return fail(MLA_ERR_NULL, "z_off and workspace are required");
+  if (!aligned16(z_off)) return fail(MLA_ERR_SHAPE, "z_off must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return fail(MLA_ERR_SHAPE, "workspace must be 256-byte aligned");
+  if (ws_bytes < L.total)
+    return fail(MLA_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, L.total);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const size_t z_bytes = (size_t)N * geom->d_model * (out_dtype == MLA_BF16 ? 2 : 4);
+  if (hpg == 1) {   // no Local heads: the artifact is zero
+    const hipError_t e = mla::launch_fill_zero(z_off, z_bytes, s);
+    return e == hipSuccess ? MLA_OK : hip_fail(e, "fill kernel");
+  }
+  if (kv == nullptr || q_loc == nullptr || w_o == nullptr) return fail(MLA_ERR_NULL, "kv, q_loc and w_o are required");
+  if (!aligned16(kv) || !aligned16(q_loc) || !aligned16(w_o))
+    return fail(MLA_ERR_SHAPE, "kv, q_loc and w_o must be 16-byte aligned");
+  if ((st = upload_plan(L.plan, workspace, s)) != MLA_OK) return st;
+
+  unsigned char* ws = reinterpret_cast<unsigned char*>(workspace);
+  mla::AttendArgs a{};
+  a.kv = kv;
+  a.q_glob = q_loc;   // unused: the plan holds no Global items
+  a.q_loc = q_loc;
+  a.ws = ws;
+  a.n_rows = N;
+  a.n_slots = L.plan.hdr.n_slots;
+  a.n_items = L.plan.hdr.n_items;
+  a.n_prot = (int32_t)N;
+  a.n_groups = geom->n_groups;
+  a.n_local = geom->n_groups * (hpg - 1);
+  a.d_latent = geom->d_latent;
+  a.d_rope = geom->d_rope;
+  a.scale_log2 = geom->softmax_scale * 1.4426950408889634f;
+  a.local_slot_base = 0;
+  a.out_bf16 = reinterpret_cast<uint16_t*>(ws + L.off_o);
+  a.hdr = L.plan.hdr;
+  hipError_t e = mla::launch_attend(a, s);
+  if (e != hipSuccess) return hip_fail(e, "attention kernel");
+
+  mla::OprojArgs op{};
+  op.o_glob = nullptr;
+  op.o_loc = ws + L.off_o;
+  op.prot_rows = reinterpret_cast<const int32_t*>(ws + L.plan.hdr.off_prot);   // identity row list
+  op.w_o = w_o;
+  op.z_off = nullptr;
+  op.z = reinterpret_cast<float*>(z_off);
+  op.n_rows = N;
+  op.n_prot = (int32_t)N;
+  op.n_heads = geom->n_heads;
+  op.n_groups = geom->n_groups;
+  op.d_latent = geom->d_latent;
+  op.d_model = geom->d_model;
+  op.n_pg = geom->n_proj_groups;
+  op.z_bf16 = out_dtype == MLA_BF16 ? 1 : 0;
+  for (int g = 0; g < geom->n_groups; ++g) op.glob_head[g] = glob_head[g];
+  e = mla::launch_oproj(op, 1, s);
+  if (e != hipSuccess) return hip_fail(e, "o-proj kernel");
   return MLA_OK;
 }
 

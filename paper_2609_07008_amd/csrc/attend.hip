@@ -160,7 +160,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   } else {
     row = prot[hr / a.n_local];
     qsrc = (const uint16_t*)a.q_loc + hr * C::D;
-    slot = a.n_rows * a.n_groups + hr;
+    slot = a.local_slot_base + hr;
   }
   const int64_t t_pos = own.req_offset + (row - own.kv_start);
 
@@ -487,8 +487,19 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   lane_halves(l_run, lx, ly);
   if (!valid) return;
   const float l_tot = lx + ly;
-  const int64_t pidx = a.part_ptr[slot] + it.chunk;
   const float inv = 1.f / l_tot;
+  if (a.out_bf16 != nullptr) {
+    // one chunk per slot (the offline producer): the head output itself, in bf16
+    uint16_t* ob = a.out_bf16 + slot * DC;
+#pragma unroll
+    for (int d = 0; d < C::OB; ++d)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        *(u32x2*)(ob + d * 32 + half * 4 + 8 * i) = u32x2{pack_bf16x2(o[d][4 * i] * inv, o[d][4 * i + 1] * inv),
+                                                          pack_bf16x2(o[d][4 * i + 2] * inv, o[d][4 * i + 3] * inv)};
+    return;
+  }
+  const int64_t pidx = a.part_ptr[slot] + it.chunk;
   float* dst = a.part_o + pidx * DC;
 #pragma unroll
   for (int d = 0; d < C::OB; ++d)

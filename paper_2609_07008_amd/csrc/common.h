@@ -99,6 +99,9 @@ struct AttendArgs {
   int32_t d_latent;
   int32_t d_rope;
   float scale_log2;          // softmax_scale * log2(e)
+  int64_t local_slot_base;   // slot of Local head-row 0: n_rows * n_groups, or 0 without Global slots
+  uint16_t* out_bf16;        // if set: one chunk per slot, normalized O written here as bf16
+                             // [slots, d_latent] (part_o / part_lse unused)
   PlanHeader hdr;            // copy of the plan header (offsets)
 };
 
@@ -123,10 +126,13 @@ struct OprojArgs {
   int32_t d_latent;
   int32_t d_model;
   int32_t n_pg;
+  int32_t z_bf16;            // 1: z is bf16 (Local pass only), 0: f32
   int32_t glob_head[kMaxGroups];
 };
 
-hipError_t launch_oproj(const OprojArgs& a, hipStream_t s);
+// passes: bit 0 = Local heads over the protected rows, bit 1 = Global heads over all rows
+hipError_t launch_oproj(const OprojArgs& a, int passes, hipStream_t s);
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 
 // ----------------------------------------------------------------------------
 // device helpers

@@ -12,6 +12,8 @@
 // straddles two heads, so the B operand is gathered per tile by head.
 #include "common.h"
 
+#include <algorithm>
+
 namespace mla {
 
 constexpr int OP_BM = 128, OP_BN = 128, OP_BK = 32;
@@ -179,6 +181,10 @@ __global__ __launch_bounds__(256) void oproj_kernel(OprojArgs a, int m_tiles, in
         if (m0 + r >= M) continue;
         const int64_t orow = row_out[r];
         float v = acc[mi][ni][e];
+        if (PASS == 0 && a.z_bf16) {   // the artifact of the offline producer
+          ((__bf16*)a.z)[orow * a.d_model + ch] = (__bf16)v;
+          continue;
+        }
         float* dst = a.z + orow * a.d_model + ch;
         if (PASS == 1) {
           if (row_flag[r]) {
@@ -191,17 +197,32 @@ __global__ __launch_bounds__(256) void oproj_kernel(OprojArgs a, int m_tiles, in
     }
 }
 
-hipError_t launch_oproj(const OprojArgs& a, hipStream_t s) {
+__global__ __launch_bounds__(256) void fill_zero_kernel(u32x4* p, int64_t n16) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = u32x4{0u, 0u, 0u, 0u};
+}
+
+// zero fill with a kernel (no memset node, so the call can be graph-captured);
+// p is 16-byte aligned and bytes a multiple of 16
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
+  const int64_t n16 = (int64_t)(bytes / 16);
+  if (n16 == 0) return hipSuccess;
+  const unsigned blocks = (unsigned)std::min<int64_t>((n16 + 255) / 256, 16384);
+  fill_zero_kernel<<<dim3(blocks), dim3(256), 0, s>>>((u32x4*)p, n16);
+  return hipGetLastError();
+}
+
+hipError_t launch_oproj(const OprojArgs& a, int passes, hipStream_t s) {
   const int cw = a.d_model / a.n_pg;
   const int n_tiles = (cw + OP_BN - 1) / OP_BN;
   const int hpg = a.n_heads / a.n_groups;
-  if (a.n_prot > 0 && hpg > 1) {
+  if ((passes & 1) && a.n_prot > 0 && hpg > 1) {
     const int m_tiles = (a.n_prot + OP_BM - 1) / OP_BM;
     oproj_kernel<0><<<dim3((unsigned)(m_tiles * n_tiles * a.n_pg)), dim3(256), 0, s>>>(a, m_tiles, n_tiles);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  if (a.n_rows > 0) {
+  if ((passes & 2) && a.n_rows > 0) {
     const int m_tiles = (int)((a.n_rows + OP_BM - 1) / OP_BM);
     oproj_kernel<1><<<dim3((unsigned)(m_tiles * n_tiles * a.n_pg)), dim3(256), 0, s>>>(a, m_tiles, n_tiles);
   }

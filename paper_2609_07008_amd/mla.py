@@ -20,6 +20,7 @@ MLA_BF16, MLA_F32 = 0, 1
 STATUS = {0: "MLA_OK", 1: "MLA_ERR_NULL", 2: "MLA_ERR_SHAPE", 3: "MLA_ERR_UNSUPPORTED",
           4: "MLA_ERR_SEGMENTS", 5: "MLA_ERR_ROWS", 6: "MLA_ERR_WORKSPACE", 7: "MLA_ERR_HIP"}
 EXPORTS = ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
+           "mla_offline_produce_query", "mla_offline_produce",
            "mla_status_str", "mla_last_error_detail", "mla_version")
 
 
@@ -51,7 +52,10 @@ def _load(path: str = LIB_PATH):
     lib.mla_online_attend.argtypes = [GP, SP, I32, P, I32, I64, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.mla_segment_merge.argtypes = [I64, I32, P, P, P, I32, P, P, P]
     lib.mla_sliced_oproj_add.argtypes = [GP, I64, P, P, P, P, I32, P, P, P, P]
-    for f in ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add"):
+    lib.mla_offline_produce_query.argtypes = [GP, SP, I32, ctypes.POINTER(SZ)]
+    lib.mla_offline_produce.argtypes = [GP, SP, I32, P, P, P, P, I32, P, P, SZ, P]
+    for f in ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
+              "mla_offline_produce_query", "mla_offline_produce"):
         getattr(lib, f).restype = ctypes.c_int
     lib.mla_status_str.argtypes = [ctypes.c_int]
     lib.mla_status_str.restype = ctypes.c_char_p
@@ -135,6 +139,26 @@ def sliced_oproj_add(geom, n_rows, o_glob, o_loc, glob_head, prot_rows_d, n_prot
     _check(LIB.mla_sliced_oproj_add(ctypes.byref(g), int(n_rows), _ptr(o_glob), _ptr(o_loc), _ptr(gh),
                                     _ptr(prot_rows_d), int(n_prot), _ptr(w_o), _ptr(z_off), _ptr(z),
                                     _stream(stream)))
+
+
+def offline_produce_query(geom, segs) -> int:
+    """Host-only: workspace bytes of mla_offline_produce."""
+    g = make_geom(geom)
+    sarr, ns = make_segments(segs)
+    ws = ctypes.c_size_t()
+    _check(LIB.mla_offline_produce_query(ctypes.byref(g), sarr, ns, ctypes.byref(ws)))
+    return ws.value
+
+
+def offline_produce(geom, segs, kv, q_loc, glob_head, w_o, out_dtype, z_off, workspace, stream=None):
+    """MLA-Off producer (mla_offline_produce): the Local-head artifact z_off of
+    every row.  Device tensors in and out; segs and glob_head are host arrays."""
+    g = make_geom(geom)
+    sarr, ns = make_segments(segs)
+    gh = np.ascontiguousarray(glob_head, dtype=np.int32)
+    _check(LIB.mla_offline_produce(ctypes.byref(g), sarr, ns, _ptr(kv), _ptr(q_loc), _ptr(gh), _ptr(w_o),
+                                   int(out_dtype), _ptr(z_off), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def version() -> str:
