@@ -16,12 +16,24 @@
 
 namespace mla {
 
-constexpr int OP_BM = 128, OP_BN = 128, OP_BK = 32;
-constexpr int OP_ALD = OP_BK + 8;     // padded A row (bf16): 80 B, conflict-free b128 reads
-constexpr int OP_BLD = OP_BN + 16;    // padded B row (bf16): 288 B, conflict-free transposed reads
+// Tile shapes: BM rows x BN channels per workgroup of WM x WN waves (wave tiles
+// of multiples of 32), K in steps of 32.
+constexpr int OP_BK = 32;
+constexpr int OP_ALD = OP_BK + 8;     // padded A row (bf16): 80 B, conflict-free 16-byte row reads
 
-template <int PASS>   // 0 = Local pass over protected rows, 1 = Global pass over all rows
-__global__ __launch_bounds__(256) void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
+template <int PASS, int BM, int BN, int WM, int WN>   // PASS 0 = Local over protected rows, 1 = Global
+__global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
+  constexpr int NT = WM * WN * 64;
+  // padded B row: 2*BLD = 64 mod 256 bytes, so the four k-rows that each half-wave
+  // of a transposing read touches land on disjoint 16-bank groups (all 64 banks)
+  constexpr int OP_BLD = BN + 32;
+  constexpr int TM = BM / WM, TN = BN / WN;    // wave tile
+  constexpr int MI = TM / 32, NI = TN / 32;     // 32x32 MFMA blocks per wave
+  constexpr int A_CH = BM * OP_BK / 8 / NT;     // 16-byte chunks per thread and K step
+  constexpr int B_CH = OP_BK * BN / 8 / NT;
+  static_assert(TM % 32 == 0 && TN % 32 == 0 && A_CH >= 1 && B_CH >= 1, "tile shape");
+  static_assert(((2 * OP_BLD) % 256) == 64, "B row padding");
+  constexpr int OP_BM = BM, OP_BN = BN;
   __shared__ __attribute__((aligned(16))) uint16_t As[2][OP_BM * OP_ALD];
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][OP_BK * OP_BLD];
   __shared__ int row_flag[OP_BM];
@@ -49,8 +61,8 @@ __global__ __launch_bounds__(256) void oproj_kernel(OprojArgs a, int m_tiles, in
   const int64_t acol = PASS == 0 ? (int64_t)pg * gpp * (hpg - 1) * DC : (int64_t)pg * gpp * DC;
   const uint16_t* W = (const uint16_t*)a.w_o + (int64_t)pg * heads_pp * DC * cw;
 
-  if (tid < OP_BM) {
-    const int64_t m = m0 + tid;
+  for (int i = tid; i < OP_BM; i += NT) {
+    const int64_t m = m0 + i;
     int flag = 0, orow = -1;
     if (m < M) {
       if (PASS == 0) {
@@ -66,8 +78,8 @@ __global__ __launch_bounds__(256) void oproj_kernel(OprojArgs a, int m_tiles, in
         flag = (lo < a.n_prot && a.prot_rows[lo] == (int)m) ? 1 : 0;
       }
     }
-    row_flag[tid] = flag;
-    row_out[tid] = orow;
+    row_flag[i] = flag;
+    row_out[i] = orow;
   }
 
   // weight row of K index k (k is a multiple of 32 inside one head block)
@@ -84,11 +96,11 @@ __global__ __launch_bounds__(256) void oproj_kernel(OprojArgs a, int m_tiles, in
     return (int64_t)hl * DC + d;
   };
 
-  u32x4 ra[2], rb[2];
+  u32x4 ra[A_CH], rb[B_CH];
   auto load_tiles = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + 256 * i;
+    for (int i = 0; i < A_CH; ++i) {
+      const int c = tid + NT * i;
       const int r = c >> 2, cc = c & 3;
       int64_t m = m0 + r;
       if (m >= M) m = M - 1;
@@ -96,9 +108,9 @@ __global__ __launch_bounds__(256) void oproj_kernel(OprojArgs a, int m_tiles, in
     }
     const int64_t wr = w_row(k0);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + 256 * i;
-      const int kr = c >> 4, cc = c & 15;
+    for (int i = 0; i < B_CH; ++i) {
+      const int c = tid + NT * i;
+      const int kr = c / (OP_BN / 8), cc = c % (OP_BN / 8);
       const int n = n0 + cc * 8;
       if (n < cw)
         rb[i] = *(const u32x4*)(W + (wr + kr) * cw + n);
@@ -108,22 +120,26 @@ __global__ __launch_bounds__(256) void oproj_kernel(OprojArgs a, int m_tiles, in
   };
   auto store_tiles = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + 256 * i;
+    for (int i = 0; i < A_CH; ++i) {
+      const int c = tid + NT * i;
       *(u32x4*)(&As[buf][(c >> 2) * OP_ALD + (c & 3) * 8]) = ra[i];
-      *(u32x4*)(&Bs[buf][(c >> 4) * OP_BLD + (c & 15) * 8]) = rb[i];
+    }
+#pragma unroll
+    for (int i = 0; i < B_CH; ++i) {
+      const int c = tid + NT * i;
+      *(u32x4*)(&Bs[buf][(c / (OP_BN / 8)) * OP_BLD + (c % (OP_BN / 8)) * 8]) = rb[i];
     }
   };
 
-  f32x16 acc[2][2];
+  f32x16 acc[MI][NI];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NI; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   const int half = lane >> 5, l32 = lane & 31;
   const int q = lane >> 4, j16 = lane & 15;
 
@@ -136,17 +152,17 @@ __global__ __launch_bounds__(256) void oproj_kernel(OprojArgs a, int m_tiles, in
     if (it + 1 < nk) load_tiles((it + 1) * OP_BK);
 #pragma unroll
     for (int ks = 0; ks < OP_BK / 16; ++ks) {
-      bf16x8 af[2], bfr[2];
+      bf16x8 af[MI], bfr[NI];
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
-        af[mi] = *(const bf16x8*)(&As[buf][(wm * 64 + mi * 32 + l32) * OP_ALD + ks * 16 + half * 8]);
+      for (int mi = 0; mi < MI; ++mi)
+        af[mi] = *(const bf16x8*)(&As[buf][(wm * TM + mi * 32 + l32) * OP_ALD + ks * 16 + half * 8]);
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
+      for (int ni = 0; ni < NI; ++ni) {
         // transposed LDS reads: lane (r*4+cb) of each 16-lane group addresses
         // k-row kb+r, columns n+cb*4..; lane j then holds column n+j of rows kb..kb+3
         const int r = j16 >> 2, cb = j16 & 3;
         const int kb = ks * 16 + (q >> 1) * 8;
-        const int n = wn * 64 + ni * 32 + (q & 1) * 16 + cb * 4;
+        const int n = wn * TN + ni * 32 + (q & 1) * 16 + cb * 4;
         const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
             (MLA_LDS bf16x4*)(&Bs[buf][(kb + r) * OP_BLD + n]));
         const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
@@ -154,9 +170,9 @@ __global__ __launch_bounds__(256) void oproj_kernel(OprojArgs a, int m_tiles, in
         bfr[ni] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       }
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
+      for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
+        for (int ni = 0; ni < NI; ++ni)
           acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bfr[ni], acc[mi][ni], 0, 0, 0);
     }
     __syncthreads();
@@ -169,15 +185,15 @@ __global__ __launch_bounds__(256) void oproj_kernel(OprojArgs a, int m_tiles, in
   // epilogue: lane holds column l32 of each 32x32 block, rows half*4 + 8i + j
   const uint16_t* zoff = (const uint16_t*)a.z_off;
 #pragma unroll
-  for (int mi = 0; mi < 2; ++mi)
+  for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
-      const int n = n0 + wn * 64 + ni * 32 + l32;
+    for (int ni = 0; ni < NI; ++ni) {
+      const int n = n0 + wn * TN + ni * 32 + l32;
       if (n >= cw) continue;
       const int64_t ch = (int64_t)pg * cw + n;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int r = wm * 64 + mi * 32 + half * 4 + (e >> 2) * 8 + (e & 3);
+        const int r = wm * TM + mi * 32 + half * 4 + (e >> 2) * 8 + (e & 3);
         if (m0 + r >= M) continue;
         const int64_t orow = row_out[r];
         float v = acc[mi][ni][e];
@@ -212,21 +228,26 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_oproj(const OprojArgs& a, int passes, hipStream_t s) {
+template <int PASS>
+hipError_t launch_pass(const OprojArgs& a, int64_t M, hipStream_t s) {
+  // 128 x 128 tiles, 4 waves (2 x 2 wave tiles of 64 x 64): about 42 KB of LDS, so
+  // three workgroups share a CU and their loads overlap each other's MFMA work
   const int cw = a.d_model / a.n_pg;
-  const int n_tiles = (cw + OP_BN - 1) / OP_BN;
+  const int n_tiles = (cw + 127) / 128;
+  const int m_tiles = (int)((M + 127) / 128);
+  oproj_kernel<PASS, 128, 128, 2, 2><<<dim3((unsigned)(m_tiles * n_tiles * a.n_pg)), dim3(256), 0, s>>>(
+      a, m_tiles, n_tiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_oproj(const OprojArgs& a, int passes, hipStream_t s) {
   const int hpg = a.n_heads / a.n_groups;
   if ((passes & 1) && a.n_prot > 0 && hpg > 1) {
-    const int m_tiles = (a.n_prot + OP_BM - 1) / OP_BM;
-    oproj_kernel<0><<<dim3((unsigned)(m_tiles * n_tiles * a.n_pg)), dim3(256), 0, s>>>(a, m_tiles, n_tiles);
-    hipError_t e = hipGetLastError();
+    const hipError_t e = launch_pass<0>(a, a.n_prot, s);
     if (e != hipSuccess) return e;
   }
-  if ((passes & 2) && a.n_rows > 0) {
-    const int m_tiles = (int)((a.n_rows + OP_BM - 1) / OP_BM);
-    oproj_kernel<1><<<dim3((unsigned)(m_tiles * n_tiles * a.n_pg)), dim3(256), 0, s>>>(a, m_tiles, n_tiles);
-  }
-  return hipGetLastError();
+  if ((passes & 2) && a.n_rows > 0) return launch_pass<1>(a, a.n_rows, s);
+  return hipSuccess;
 }
 
 }  // namespace mla
