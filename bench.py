@@ -245,6 +245,40 @@ def offline_producer(wl, torch, stream, reps: int = 2, seed: int = 70080):
             "inputs": f"device-drawn, torch.Generator seed {seed}"}
 
 
+def protected_set(wl, torch, stream, budgets=(0.10, 0.20, 0.25), reps: int = 5, seed: int = 70080):
+    """mla_protected_rows (eq:protected) on the workload's segment table: query
+    block, 1 % dirty rows, first/last 128 rows of relocated segments, the 32K
+    tail, and the Indexer top-up to each budget level.  Indexer scores are
+    seeded N(0, 1) draws; returns the median time and |A| per budget."""
+    from paper_2609_07008_amd import mla
+    segs = np.asarray(wl.segs, dtype=np.int64)
+    n = wl.n_rows
+    q = int(np.argmax(segs[:, 2]))
+    rng = np.random.default_rng(seed)
+    flags = np.zeros(n, dtype=np.uint8)
+    flags[rng.choice(n, size=n // 100, replace=False)] |= 2
+    fl = torch.from_numpy(flags).cuda()
+    sc = torch.from_numpy(rng.standard_normal(n).astype(np.float32)).cuda()
+    ws = torch.empty(mla.protected_rows_query(segs), dtype=torch.uint8, device="cuda")
+    out = torch.empty(n, dtype=torch.int32, device="cuda")
+    cnt = torch.empty(1, dtype=torch.int32, device="cuda")
+    res = {}
+    for b in budgets:
+        args = (segs, q, 128, 32768, b, fl, sc, out, cnt, ws)
+        mla.protected_rows(*args, stream=stream)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            mla.protected_rows(*args, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        res[f"{b:.2f}"] = {"us": round(float(np.median(ts)) * 1e3, 1), "protected": int(cnt.item())}
+    return {"rows": n, "budgets": res, "edge_rows": 128, "tail_rows": 32768, "dirty_rows": n // 100}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -354,6 +388,7 @@ def main():
         out["merge_per_segment"] = merge_per_segment(wl, torch, stream)
     if not args.no_offline_producer:
         out["offline_producer"] = offline_producer(wl, torch, stream)
+    out["protected_set"] = protected_set(wl, torch, stream)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -228,6 +228,49 @@ mla_status mla_offline_produce(const mla_geom* geom, const mla_segment* segs, in
                                const void* w_o, int32_t out_dtype, void* z_off, void* workspace,
                                size_t ws_bytes, void* stream);
 
+/* ----------------------------------------------------------------------------
+ * mla_protected_rows -- the protected token-row set of Sec. 2.3 (eq:protected):
+ *   A = Q u N u D u B_edge u I_top u T_tail
+ * as an ascending list of storage rows, ready to be copied to the host as the
+ * prot_rows argument of mla_online_attend.
+ *   Q       rows of the query segment (cfg->query_seg, -1 for none);
+ *   N, D    rows flagged new (bit 0 of row_flags) or dirty (bit 1);
+ *   B_edge  the first and last cfg->edge_rows rows of every relocated segment,
+ *           i.e. every non-query segment whose request offset is not 0;
+ *   T_tail  rows whose true request position is among the last cfg->tail_rows;
+ *   I_top   the highest-scoring candidate rows outside the sets above, where
+ *           candidates are the rows that have an artifact (neither query nor
+ *           new rows): enough of them that round(cfg->budget * |candidates|)
+ *           candidates are protected (none when the other sets already reach
+ *           it); the budget is the controller's level (0.10, 0.20 or 0.25 in the
+ *           paper).  Scores rank by IEEE-754 totalOrder, descending; equal
+ *           scores go to the lower row; rounding is half up.
+ *
+ *   segs, n_segs   segment table as for mla_online_attend (host).
+ *   cfg            host; edge_rows >= 0, tail_rows >= 0, 0 <= budget <= 1.
+ *   row_flags      [N] uint8 device, or NULL (no new or dirty rows).
+ *   index_scores   [N] float device (the Indexer's score of each row), or NULL
+ *                  (every score equal: I_top then takes the lowest rows).
+ *   prot_rows      [N] int32 device, written with the |A| protected rows.
+ *   n_prot         [1] int32 device, written with |A|.
+ *   workspace      device, 256-byte aligned, mla_protected_rows_query bytes.
+ * Errors as for mla_online_attend; the result is exact (integer), independent
+ * of the launch configuration.
+ * ------------------------------------------------------------------------- */
+typedef struct mla_protect_cfg {
+  int32_t query_seg;   /* index of the query segment in segs, or -1                 */
+  int32_t edge_rows;   /* B: first / last rows of each relocated segment (128)      */
+  int64_t tail_rows;   /* T: most recent rows in request order (32768)              */
+  double budget;       /* protected share of candidate rows (0.10, 0.20, 0.25)      */
+} mla_protect_cfg;
+
+mla_status mla_protected_rows_query(const mla_segment* segs, int32_t n_segs, size_t* ws_bytes);
+
+mla_status mla_protected_rows(const mla_segment* segs, int32_t n_segs, const mla_protect_cfg* cfg,
+                              const uint8_t* row_flags, const float* index_scores,
+                              int32_t* prot_rows, int32_t* n_prot, void* workspace, size_t ws_bytes,
+                              void* stream);
+
 /* Static description of a status code. */
 const char* mla_status_str(mla_status s);
 

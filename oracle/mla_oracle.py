@@ -34,6 +34,10 @@ What it computes, and where the paper defines it:
   statement; the function itself is pinned by the prefix-document identity).
 * ``enumerate_plan`` -- the integer bookkeeping: which segments each output
   slot sees, how they are cut into partials, and the protected-row flags.
+* ``protected_rows`` -- the protected token-row set of Sec. 2.3 (eq:protected):
+  query rows, new and dirty rows, the first and last rows of every relocated
+  segment, the recent tail, and the Indexer's top rows, which top the
+  protected share of the candidate rows up to the controller's budget.
 
 Readings where the paper is silent: V is the latent itself, so the inverse
 output RoPE and RestorePhase are the identity; a key is visible to a row iff
@@ -374,3 +378,52 @@ def enumerate_plan(segs, n_groups: int, heads_per_group: int, prot_rows, split_k
     row_src = np.zeros(n, dtype=np.uint8)
     row_src[prot] = 1
     return row_src, part_ptr, part_seg
+
+
+# ----------------------------------------------------------------------------
+# protected token-row set (Sec. 2.3, eq:protected)
+# ----------------------------------------------------------------------------
+def total_order_key(scores) -> np.ndarray:
+    """uint32 keys that sort float32 values by the IEEE-754 totalOrder predicate
+    (-0 below +0): the sign-magnitude bit pattern mapped to an unsigned order."""
+    u = np.ascontiguousarray(scores, dtype=np.float32).view(np.uint32)
+    neg = (u >> np.uint32(31)) != 0
+    return np.where(neg, ~u, u | np.uint32(0x80000000)).astype(np.uint32)
+
+
+def protected_rows(segs, query_seg: int, row_flags, scores, edge: int = 128, tail: int = 32768,
+                   budget: float = 0.10) -> np.ndarray:
+    """A = Q u N u D u B_edge u I_top u T_tail (eq:protected), as sorted storage rows.
+
+    Q: rows of the query segment.  N, D: rows flagged new (bit 0 of row_flags) or
+    dirty (bit 1).  B_edge: the first and last `edge` rows of every relocated
+    segment (a non-query segment whose request offset is not 0).  T_tail: rows
+    whose true request position is among the last `tail` of the request.
+    Candidates are the rows that have an artifact: neither query nor new rows.
+    The controller's budget is a share of the candidates: I_top adds the
+    highest-scoring candidates outside the other sets until
+    round(budget * |candidates|) candidates are protected (nothing when the
+    other sets already reach it).  Scores rank by IEEE-754 totalOrder,
+    descending; equal scores go to the lower row.  Rounding is half up."""
+    segs = np.asarray(segs, dtype=np.int64)
+    seg, u, pos = row_geometry(segs)
+    n = seg.shape[0]
+    flags = np.asarray(row_flags, dtype=np.uint8)
+    new = (flags & 1) != 0
+    dirty = (flags & 2) != 0
+    q = seg == int(query_seg)
+    length = segs[seg, 1]
+    relocated = (segs[seg, 2] != 0) & ~q
+    edge_rows = relocated & ((u < edge) | (u >= length - edge))
+    recent = pos >= n - tail
+    base = q | new | dirty | edge_rows | recent
+    cand = ~q & ~new
+    target = int(np.floor(budget * int(cand.sum()) + 0.5))
+    k = max(0, target - int((base & cand).sum()))
+    elig = np.flatnonzero(cand & ~base)
+    key = total_order_key(np.asarray(scores, dtype=np.float32)[elig])
+    order = np.lexsort((elig, -key.astype(np.int64)))   # key descending, then row ascending
+    sel = base.copy()
+    sel[elig[order[:k]]] = True
+    return np.flatnonzero(sel).astype(np.int32)
+

@@ -594,4 +594,106 @@ mla_status mla_offline_produce(const mla_geom* geom, const mla_segment* segs, in
   return MLA_OK;
 }
 
+// ---------------------------------------------------------------------------
+// protected token-row set (eq:protected)
+// ---------------------------------------------------------------------------
+namespace {
+
+struct ProtectLayout {
+  Plan table;   // storage-ordered segment table, uploaded like a plan
+  int64_t n_rows = 0;
+  int64_t off_kv = 0, off_len = 0, off_req = 0, off_orig = 0, off_key = 0, off_flag = 0;
+  size_t total = 0;
+};
+
+mla_status protect_layout(const mla_segment* segs, int32_t n_segs, bool want_blob, ProtectLayout* L) {
+  int64_t N = 0;
+  const mla_status st = check_segments(segs, n_segs, &N);
+  if (st != MLA_OK) return st;
+  L->n_rows = N;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, 256);
+    return (int64_t)o;
+  };
+  L->off_kv = take(sizeof(int64_t) * n_segs);
+  L->off_len = take(sizeof(int64_t) * n_segs);
+  L->off_req = take(sizeof(int64_t) * n_segs);
+  L->off_orig = take(sizeof(int32_t) * n_segs);
+  const size_t table_bytes = off;
+  L->off_key = take(sizeof(uint64_t) * (size_t)N);
+  L->off_flag = take((size_t)N);
+  L->total = off;
+  if (!want_blob) return MLA_OK;
+  std::vector<int32_t> storage(n_segs);
+  std::iota(storage.begin(), storage.end(), 0);
+  std::sort(storage.begin(), storage.end(), [&](int32_t x, int32_t y) { return segs[x].kv_start < segs[y].kv_start; });
+  L->table.blob.assign(table_bytes, 0);
+  unsigned char* B = L->table.blob.data();
+  for (int32_t i = 0; i < n_segs; ++i) {
+    const mla_segment& sg = segs[storage[i]];
+    reinterpret_cast<int64_t*>(B + L->off_kv)[i] = sg.kv_start;
+    reinterpret_cast<int64_t*>(B + L->off_len)[i] = sg.length;
+    reinterpret_cast<int64_t*>(B + L->off_req)[i] = sg.req_offset;
+    reinterpret_cast<int32_t*>(B + L->off_orig)[i] = storage[i];
+  }
+  return MLA_OK;
+}
+
+}  // namespace
+
+mla_status mla_protected_rows_query(const mla_segment* segs, int32_t n_segs, size_t* ws_bytes) {
+  g_detail.clear();
+  if (ws_bytes == nullptr) return fail(MLA_ERR_NULL, "ws_bytes is NULL");
+  ProtectLayout L;
+  const mla_status st = protect_layout(segs, n_segs, false, &L);
+  if (st != MLA_OK) return st;
+  *ws_bytes = L.total;
+  return MLA_OK;
+}
+
+mla_status mla_protected_rows(const mla_segment* segs, int32_t n_segs, const mla_protect_cfg* cfg,
+                              const uint8_t* row_flags, const float* index_scores, int32_t* prot_rows,
+                              int32_t* n_prot, void* workspace, size_t ws_bytes, void* stream) {
+  g_detail.clear();
+  if (cfg == nullptr) return fail(MLA_ERR_NULL, "cfg is NULL");
+  ProtectLayout L;
+  mla_status st = protect_layout(segs, n_segs, true, &L);
+  if (st != MLA_OK) return st;
+  if (cfg->query_seg < -1 || cfg->query_seg >= n_segs)
+    return fail(MLA_ERR_SHAPE, "query_seg %d outside [-1, %d)", cfg->query_seg, n_segs);
+  if (cfg->edge_rows < 0 || cfg->tail_rows < 0)
+    return fail(MLA_ERR_SHAPE, "edge_rows %d and tail_rows %lld must be >= 0", cfg->edge_rows,
+                (long long)cfg->tail_rows);
+  if (!(cfg->budget >= 0.0 && cfg->budget <= 1.0)) return fail(MLA_ERR_SHAPE, "budget must lie in [0, 1]");
+  if (prot_rows == nullptr || n_prot == nullptr || workspace == nullptr)
+    return fail(MLA_ERR_NULL, "prot_rows, n_prot and workspace are required");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return fail(MLA_ERR_SHAPE, "workspace must be 256-byte aligned");
+  if (ws_bytes < L.total) return fail(MLA_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, L.total);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if ((st = upload_plan(L.table, workspace, s)) != MLA_OK) return st;
+  mla::ProtectArgs a{};
+  a.ws = reinterpret_cast<const unsigned char*>(workspace);
+  a.row_flags = row_flags;
+  a.scores = index_scores;
+  a.prot_rows = prot_rows;
+  a.n_prot = n_prot;
+  a.n_rows = L.n_rows;
+  a.tail_rows = cfg->tail_rows;
+  a.off_kv = L.off_kv;
+  a.off_len = L.off_len;
+  a.off_req = L.off_req;
+  a.off_orig = L.off_orig;
+  a.off_key = L.off_key;
+  a.off_flag = L.off_flag;
+  a.n_segs = n_segs;
+  a.query_seg = cfg->query_seg;
+  a.edge_rows = cfg->edge_rows;
+  a.budget = cfg->budget;
+  const hipError_t e = mla::launch_protect(a, s);
+  if (e != hipSuccess) return hip_fail(e, "protected-row kernels");
+  return MLA_OK;
+}
+
 }  // extern "C"

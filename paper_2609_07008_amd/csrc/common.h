@@ -134,6 +134,26 @@ struct OprojArgs {
 hipError_t launch_oproj(const OprojArgs& a, int passes, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 
+// protected token-row set (eq:protected); ws holds the storage-ordered segment
+// table, the per-row keys and the per-row flags
+struct ProtectArgs {
+  const unsigned char* ws;
+  const uint8_t* row_flags;    // [N] bit 0 new, bit 1 dirty (may be null)
+  const float* scores;         // [N] Indexer scores (may be null: all equal)
+  int32_t* prot_rows;          // [N] out: protected rows, ascending
+  int32_t* n_prot;             // [1] out
+  int64_t n_rows;
+  int64_t tail_rows;
+  int64_t off_kv, off_len, off_req, off_orig, off_key, off_flag;
+  int32_t n_segs;
+  int32_t query_seg;
+  int32_t edge_rows;
+  int32_t pad;
+  double budget;
+};
+
+hipError_t launch_protect(const ProtectArgs& a, hipStream_t s);
+
 // ----------------------------------------------------------------------------
 // device helpers
 // ----------------------------------------------------------------------------

@@ -20,7 +20,7 @@ MLA_BF16, MLA_F32 = 0, 1
 STATUS = {0: "MLA_OK", 1: "MLA_ERR_NULL", 2: "MLA_ERR_SHAPE", 3: "MLA_ERR_UNSUPPORTED",
           4: "MLA_ERR_SEGMENTS", 5: "MLA_ERR_ROWS", 6: "MLA_ERR_WORKSPACE", 7: "MLA_ERR_HIP"}
 EXPORTS = ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
-           "mla_offline_produce_query", "mla_offline_produce",
+           "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query", "mla_protected_rows",
            "mla_status_str", "mla_last_error_detail", "mla_version")
 
 
@@ -41,6 +41,11 @@ class Segment(ctypes.Structure):
     _fields_ = [("kv_start", ctypes.c_int64), ("length", ctypes.c_int64), ("req_offset", ctypes.c_int64)]
 
 
+class ProtectCfg(ctypes.Structure):
+    _fields_ = [("query_seg", ctypes.c_int32), ("edge_rows", ctypes.c_int32), ("tail_rows", ctypes.c_int64),
+                ("budget", ctypes.c_double)]
+
+
 def _load(path: str = LIB_PATH):
     if not os.path.exists(path):
         raise ImportError(f"{path} is not built; run `python -m paper_2609_07008_amd.build`")
@@ -54,8 +59,11 @@ def _load(path: str = LIB_PATH):
     lib.mla_sliced_oproj_add.argtypes = [GP, I64, P, P, P, P, I32, P, P, P, P]
     lib.mla_offline_produce_query.argtypes = [GP, SP, I32, ctypes.POINTER(SZ)]
     lib.mla_offline_produce.argtypes = [GP, SP, I32, P, P, P, P, I32, P, P, SZ, P]
+    lib.mla_protected_rows_query.argtypes = [SP, I32, ctypes.POINTER(SZ)]
+    lib.mla_protected_rows.argtypes = [SP, I32, ctypes.POINTER(ProtectCfg), P, P, P, P, P, SZ, P]
     for f in ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
-              "mla_offline_produce_query", "mla_offline_produce"):
+              "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query",
+              "mla_protected_rows"):
         getattr(lib, f).restype = ctypes.c_int
     lib.mla_status_str.argtypes = [ctypes.c_int]
     lib.mla_status_str.restype = ctypes.c_char_p
@@ -159,6 +167,26 @@ def offline_produce(geom, segs, kv, q_loc, glob_head, w_o, out_dtype, z_off, wor
     _check(LIB.mla_offline_produce(ctypes.byref(g), sarr, ns, _ptr(kv), _ptr(q_loc), _ptr(gh), _ptr(w_o),
                                    int(out_dtype), _ptr(z_off), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def protected_rows_query(segs) -> int:
+    """Host-only: workspace bytes of mla_protected_rows."""
+    sarr, ns = make_segments(segs)
+    ws = ctypes.c_size_t()
+    _check(LIB.mla_protected_rows_query(sarr, ns, ctypes.byref(ws)))
+    return ws.value
+
+
+def protected_rows(segs, query_seg, edge_rows, tail_rows, budget, row_flags, scores, prot_rows, n_prot,
+                   workspace, stream=None):
+    """The protected token-row set (mla_protected_rows) into the device tensors
+    prot_rows [N] int32 and n_prot [1] int32; row_flags and scores are device
+    tensors or None."""
+    sarr, ns = make_segments(segs)
+    cfg = ProtectCfg(int(query_seg), int(edge_rows), int(tail_rows), float(budget))
+    _check(LIB.mla_protected_rows(sarr, ns, ctypes.byref(cfg), _ptr(row_flags), _ptr(scores), _ptr(prot_rows),
+                                  _ptr(n_prot), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                  _stream(stream)))
 
 
 def version() -> str:

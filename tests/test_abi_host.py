@@ -165,3 +165,61 @@ def test_merge_and_oproj_reject(mla):
     assert call(g, wl.n_rows, gh, 2, None) == 1                           # z_off needed
     g2 = mla.make_geom(_geom(wl, d_model=40, n_proj_groups=2))
     assert call(g2, wl.n_rows, gh, 2, a) == 3                             # 20 channels per group
+
+
+def test_offline_produce_rejects(mla):
+    """mla_offline_produce validates everything before its first HIP call."""
+    wl = _tiny()
+    g = mla.make_geom(wl.geom)
+    sarr, ns = mla.make_segments(wl.segs)
+    P = ctypes.c_void_p
+    ws = mla.offline_produce_query(wl.geom, wl.segs)
+    hl = wl.geom.heads_per_group - 1
+    assert ws >= wl.n_rows * wl.geom.n_groups * hl * wl.geom.d_latent * 2   # holds the bf16 head outputs
+    gh = np.asarray(wl.glob_head, dtype=np.int32)
+    ok = 1 << 20
+
+    def call(kv, q, gh_arr, w, dt, z, wsp, wsb):
+        return mla.LIB.mla_offline_produce(ctypes.byref(g), sarr, ns, P(kv), P(q), gh_arr.ctypes.data_as(P), P(w),
+                                           dt, P(z), P(wsp), wsb, None)
+    assert call(ok, ok, gh, ok, 7, ok, ok, ws) == 2                 # out_dtype
+    bad = gh.copy()
+    bad[0] = wl.geom.heads_per_group
+    assert call(ok, ok, bad, ok, 0, ok, ok, ws) == 2                # Global head outside its group
+    assert call(ok, ok, gh, ok, 0, 0, ok, ws) == 1                  # z_off missing
+    assert call(ok, ok, gh, ok, 0, ok + 8, ok, ws) == 2             # z_off misaligned
+    assert call(ok, ok, gh, ok, 0, ok, ok + 16, ws) == 2            # workspace not 256-byte aligned
+    assert call(ok, ok, gh, ok, 0, ok, ok, ws - 256) == 6           # workspace too small
+    assert call(0, ok, gh, ok, 0, ok, ok, ws) == 1                  # kv missing
+
+
+def test_protected_rows_rejects(mla):
+    """mla_protected_rows validates its configuration before any HIP call, and its
+    workspace holds one 8-byte key and one flag byte per row."""
+    wl = _tiny()
+    sarr, ns = mla.make_segments(wl.segs)
+    P = ctypes.c_void_p
+    ws = mla.protected_rows_query(wl.segs)
+    assert ws >= 9 * wl.n_rows
+    ok = 1 << 20
+
+    def call(q, edge, tail, budget, out, wsp, wsb, cfg_null=False):
+        cfg = mla.ProtectCfg(q, edge, tail, budget)
+        return mla.LIB.mla_protected_rows(sarr, ns, None if cfg_null else ctypes.byref(cfg), None, None, P(out),
+                                          P(out), P(wsp), wsb, None)
+    nseg = int(np.asarray(wl.segs).shape[0])
+    assert call(0, 4, 8, 0.1, ok, ok, ws, cfg_null=True) == 1
+    assert call(nseg, 4, 8, 0.1, ok, ok, ws) == 2                   # query segment out of range
+    assert call(-2, 4, 8, 0.1, ok, ok, ws) == 2
+    assert call(0, -1, 8, 0.1, ok, ok, ws) == 2                     # negative edge
+    assert call(0, 4, -8, 0.1, ok, ok, ws) == 2                     # negative tail
+    assert call(0, 4, 8, 1.5, ok, ok, ws) == 2                      # budget above 1
+    assert call(0, 4, 8, float("nan"), ok, ok, ws) == 2             # budget NaN
+    assert call(0, 4, 8, 0.1, 0, ok, ws) == 1                       # outputs missing
+    assert call(0, 4, 8, 0.1, ok, ok + 16, ws) == 2                 # workspace not 256-byte aligned
+    assert call(0, 4, 8, 0.1, ok, ok, ws - 256) == 6                # workspace too small
+    bad = np.asarray(wl.segs, dtype=np.int64).copy()
+    bad[0, 1] += 1                                                  # no longer tiles the rows
+    sb, nb = mla.make_segments(bad)
+    cfg = mla.ProtectCfg(0, 4, 8, 0.1)
+    assert mla.LIB.mla_protected_rows(sb, nb, ctypes.byref(cfg), None, None, P(ok), P(ok), P(ok), ws, None) == 4

@@ -513,3 +513,90 @@ def test_planted_mistake_is_caught(name, monkeypatch):
 
 def test_unmutated_checks_pass():
     _all_checks()
+
+
+# ----------------------------------------------------------------------------
+# protected token-row set (Sec. 2.3, eq:protected)
+# ----------------------------------------------------------------------------
+def _protect_case(seed=0, n_docs=5, qlen=7, edge=3, tail=9, budget=0.3, ties=False):
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(2, 14, size=n_docs).tolist()
+    perm = rng.permutation(n_docs).tolist()
+    wl = make_custom(lens, req_perm=perm, tq=qlen, H=4, G=2, seed=seed)
+    segs = np.asarray(wl.segs, dtype=np.int64)
+    n = int(segs[:, 1].sum())
+    flags = np.zeros(n, dtype=np.uint8)
+    flags[rng.choice(n, size=3, replace=False)] |= 1
+    flags[rng.choice(n, size=3, replace=False)] |= 2
+    scores = rng.standard_normal(n).astype(np.float32)
+    if ties:
+        scores = np.round(scores).astype(np.float32)
+    return segs, n_docs, flags, scores, edge, tail, budget
+
+
+def _fixed_sets_by_rows(segs, qseg, flags, edge, tail):
+    """The fixed sets of eq:protected, row by row from the segment table."""
+    n = int(segs[:, 1].sum())
+    base, cand = set(), set()
+    for s, (ks, ln, ro) in enumerate(segs):
+        for u in range(int(ln)):
+            r = int(ks) + u
+            t = int(ro) + u
+            is_q = s == qseg
+            is_new = bool(flags[r] & 1)
+            in_b = (not is_q) and ro != 0 and (u < edge or u >= ln - edge)
+            if is_q or is_new or (flags[r] & 2) or in_b or t >= n - tail:
+                base.add(r)
+            if not is_q and not is_new:
+                cand.add(r)
+    return base, cand
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("ties", [False, True])
+def test_protected_rows_definition(seed, ties):
+    segs, qseg, flags, scores, edge, tail, budget = _protect_case(seed, ties=ties)
+    got = M.protected_rows(segs, qseg, flags, scores, edge, tail, budget)
+    assert got.dtype == np.int32 and np.all(np.diff(got) > 0)           # ascending, unique
+    base, cand = _fixed_sets_by_rows(segs, qseg, flags, edge, tail)
+    sel = set(got.tolist())
+    assert base <= sel                                                    # Q, N, D, B, T all kept
+    target = int(np.floor(budget * len(cand) + 0.5))
+    assert len(sel & cand) == max(target, len(base & cand))               # the budget, exactly
+    assert sel <= base | cand
+    # I_top, by counting for every eligible row how many eligible rows outrank it
+    key = M.total_order_key(scores).astype(np.int64)
+    elig = sorted(cand - base)
+    k = len(sel & cand) - len(base & cand)
+    for r in elig:
+        beaten_by = sum(1 for x in elig if key[x] > key[r] or (key[x] == key[r] and x < r))
+        assert (r in sel) == (beaten_by < k), r
+
+
+def test_protected_rows_budget_limits():
+    segs, qseg, flags, scores, edge, tail, _ = _protect_case(3)
+    base, cand = _fixed_sets_by_rows(segs, qseg, flags, edge, tail)
+    assert set(M.protected_rows(segs, qseg, flags, scores, edge, tail, 0.0).tolist()) == base
+    n = int(segs[:, 1].sum())
+    assert M.protected_rows(segs, qseg, flags, scores, edge, tail, 1.0).tolist() == list(range(n))
+    assert M.protected_rows(segs, qseg, flags, scores, edge, n, 0.0).tolist() == list(range(n))   # tail covers all
+
+
+def test_protected_rows_edges_of_relocated_segments_only():
+    # three documents: the first at request offset 0 (not relocated), a short one,
+    # a long one; no query block, no tail, no budget
+    segs = np.array([[0, 10, 0], [10, 4, 30], [14, 20, 10]], dtype=np.int64)
+    got = set(M.protected_rows(segs, -1, np.zeros(34, np.uint8), np.zeros(34, np.float32),
+                               edge=3, tail=0, budget=0.0).tolist())
+    assert got == {10, 11, 12, 13} | {14, 15, 16, 31, 32, 33}
+
+
+def test_protected_rows_total_order_ties():
+    # one relocated-free document of 6 rows; budget 1/2 of 6 candidates -> 3 rows
+    segs = np.array([[0, 6, 0]], dtype=np.int64)
+    scores = np.array([-0.0, 0.0, 1.0, 1.0, np.nan, -np.inf], dtype=np.float32)
+    got = M.protected_rows(segs, -1, np.zeros(6, np.uint8), scores, edge=0, tail=0, budget=0.5).tolist()
+    # positive NaN ranks above every number; the two 1.0 tie -> both before +0 and -0
+    assert got == [2, 3, 4]
+    got = M.protected_rows(segs, -1, np.zeros(6, np.uint8), scores, edge=0, tail=0, budget=4 / 6).tolist()
+    assert got == [1, 2, 3, 4]        # +0 ranks above -0
