@@ -602,7 +602,8 @@ namespace {
 struct ProtectLayout {
   Plan table;   // storage-ordered segment table, uploaded like a plan
   int64_t n_rows = 0;
-  int64_t off_kv = 0, off_len = 0, off_req = 0, off_orig = 0, off_key = 0, off_flag = 0;
+  int64_t off_kv = 0, off_len = 0, off_req = 0, off_orig = 0, off_ctl = 0, off_hist = 0;
+  int64_t off_key = 0, off_flag = 0, off_list = 0, off_bcnt = 0;
   size_t total = 0;
 };
 
@@ -621,9 +622,13 @@ mla_status protect_layout(const mla_segment* segs, int32_t n_segs, bool want_blo
   L->off_len = take(sizeof(int64_t) * n_segs);
   L->off_req = take(sizeof(int64_t) * n_segs);
   L->off_orig = take(sizeof(int32_t) * n_segs);
-  const size_t table_bytes = off;
+  L->off_ctl = take(mla::kProtectCtlBytes);
+  L->off_hist = take(mla::kProtectHistBytes);
+  const size_t table_bytes = off;   // uploaded: the table, then zeroed control words and histogram
   L->off_key = take(sizeof(uint64_t) * (size_t)N);
   L->off_flag = take((size_t)N);
+  L->off_list = take(sizeof(uint64_t) * (size_t)N);
+  L->off_bcnt = take(sizeof(uint64_t) * (size_t)std::max<int64_t>(1, mla::protect_count_blocks(N)));
   L->total = off;
   if (!want_blob) return MLA_OK;
   std::vector<int32_t> storage(n_segs);
@@ -674,7 +679,7 @@ mla_status mla_protected_rows(const mla_segment* segs, int32_t n_segs, const mla
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if ((st = upload_plan(L.table, workspace, s)) != MLA_OK) return st;
   mla::ProtectArgs a{};
-  a.ws = reinterpret_cast<const unsigned char*>(workspace);
+  a.ws = reinterpret_cast<unsigned char*>(workspace);
   a.row_flags = row_flags;
   a.scores = index_scores;
   a.prot_rows = prot_rows;
@@ -685,8 +690,12 @@ mla_status mla_protected_rows(const mla_segment* segs, int32_t n_segs, const mla
   a.off_len = L.off_len;
   a.off_req = L.off_req;
   a.off_orig = L.off_orig;
+  a.off_ctl = L.off_ctl;
+  a.off_hist = L.off_hist;
   a.off_key = L.off_key;
   a.off_flag = L.off_flag;
+  a.off_list = L.off_list;
+  a.off_bcnt = L.off_bcnt;
   a.n_segs = n_segs;
   a.query_seg = cfg->query_seg;
   a.edge_rows = cfg->edge_rows;

@@ -103,3 +103,12 @@ def test_protect_edge_cases(variant):
         edge = 0
     args = (segs, q, flags, scores, edge, tail, budget)
     assert np.array_equal(gpu_protect(*args), oracle(*args))
+
+
+@pytest.mark.parametrize("budget", [0.10, 0.5])
+def test_protect_many_segments(budget):
+    """More segments than the classify kernel holds in LDS (it then searches the
+    table in device memory), many short ones, ragged last block."""
+    segs, q, flags, scores = case(21, n_docs=1500, max_len=40, ties=True)
+    args = (segs, q, flags, scores, 4, 300, budget)
+    assert np.array_equal(gpu_protect(*args), oracle(*args))
