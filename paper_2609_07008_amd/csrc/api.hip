@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "common.h"
+#include "protect.h"
 
 namespace {
 

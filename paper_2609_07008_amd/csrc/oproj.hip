@@ -46,7 +46,13 @@ __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_
   const int heads_pp = a.n_heads / a.n_pg;
   const int DC = a.d_latent;
 
-  int bid = blockIdx.x;
+  // XCD-aware tile order: workgroups go to the 8 XCDs round-robin by id, so XCD x
+  // takes the contiguous tile range [x*per, (x+1)*per); the n_tiles column tiles
+  // of one row block are consecutive and share that row block in the XCD's L2
+  const int total = n_tiles * m_tiles * a.n_pg;
+  const int per = (total + 7) / 8;
+  int bid = (int)(blockIdx.x % 8) * per + (int)(blockIdx.x / 8);
+  if (bid >= total) return;
   const int nt = bid % n_tiles;
   bid /= n_tiles;
   const int mt = bid % m_tiles;
@@ -235,7 +241,8 @@ hipError_t launch_pass(const OprojArgs& a, int64_t M, hipStream_t s) {
   const int cw = a.d_model / a.n_pg;
   const int n_tiles = (cw + 127) / 128;
   const int m_tiles = (int)((M + 127) / 128);
-  oproj_kernel<PASS, 128, 128, 2, 2><<<dim3((unsigned)(m_tiles * n_tiles * a.n_pg)), dim3(256), 0, s>>>(
+  const int total = m_tiles * n_tiles * a.n_pg;
+  oproj_kernel<PASS, 128, 128, 2, 2><<<dim3((unsigned)(8 * ((total + 7) / 8))), dim3(256), 0, s>>>(
       a, m_tiles, n_tiles);
   return hipGetLastError();
 }

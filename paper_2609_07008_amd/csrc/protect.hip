@@ -29,7 +29,7 @@
 //   count     (grid)  selected rows per 2048-row block;
 //   scan      (1 WG)  exclusive offsets of the blocks and |A|;
 //   write     (grid)  each block writes its selected rows at its offset, ascending.
-#include "common.h"
+#include "protect.h"
 
 #include <algorithm>
 
