@@ -38,6 +38,12 @@ What it computes, and where the paper defines it:
   query rows, new and dirty rows, the first and last rows of every relocated
   segment, the recent tail, and the Indexer's top rows, which top the
   protected share of the candidate rows up to the controller's budget.
+* ``moe_fanout`` -- the adaptive MoE fanout of Sec. 2.4 (eq:moe): per token
+  row, the router's top-6 experts, and the smallest fanout K in {3,..,6} whose
+  normalized top-6 weights reach tau; executed experts keep their original
+  weights.  The paper fixes no precision: the integer K is decided in float32
+  (normalize by the float32 sum of the six, then accumulate in rank order),
+  as the GPU kernel decides it.
 
 Readings where the paper is silent: V is the latent itself, so the inverse
 output RoPE and RestorePhase are the identity; a key is visible to a row iff
@@ -427,3 +433,40 @@ def protected_rows(segs, query_seg: int, row_flags, scores, edge: int = 128, tai
     sel[elig[order[:k]]] = True
     return np.flatnonzero(sel).astype(np.int32)
 
+
+
+# ----------------------------------------------------------------------------
+# adaptive MoE fanout (Sec. 2.4, eq:moe)
+# ----------------------------------------------------------------------------
+def moe_fanout(router, tau: float, top_k: int = 6, min_k: int = 3):
+    """Per row of router weights p [N, E]: the top_k experts ranked by weight
+    (IEEE-754 totalOrder, descending; equal weights go to the lower expert),
+    their original weights, and the fanout
+        K = min{k in [min_k, top_k] : sum_{j<=k} p_(j) / sum_{r<=top_k} p_(r) >= tau},
+    or top_k when no k qualifies (eq:moe, with top_k = 6 and min_k = 3 in the
+    paper).  float32 throughout, in rank order: S = p_(1) + ... + p_(top_k)
+    summed left to right, p^_j = p_(j) / S, and the running sum of the p^_j is
+    compared with float32(tau).  Returns (idx [N, top_k] int32, w [N, top_k]
+    float32, K [N] int32)."""
+    p = np.ascontiguousarray(router, dtype=np.float32)
+    n, e = p.shape
+    key = total_order_key(p).astype(np.int64)
+    expert = np.broadcast_to(np.arange(e, dtype=np.int64), (n, e))
+    order = np.lexsort((expert, -key), axis=-1)           # weight descending, then expert ascending
+    idx = order[:, :top_k].astype(np.int32)
+    w = np.take_along_axis(p, order[:, :top_k], axis=1)
+    s = w[:, 0].copy()
+    for j in range(1, top_k):
+        s = (s + w[:, j]).astype(np.float32)
+    cum = np.zeros(n, dtype=np.float32)
+    k_out = np.full(n, top_k, dtype=np.int32)
+    decided = np.zeros(n, dtype=bool)
+    t = np.float32(tau)
+    with np.errstate(invalid="ignore", divide="ignore"):
+        for j in range(top_k):
+            cum = (cum + (w[:, j] / s).astype(np.float32)).astype(np.float32)
+            if j + 1 >= min_k:
+                hit = ~decided & (cum >= t)
+                k_out[hit] = j + 1
+                decided |= hit
+    return idx, w, k_out

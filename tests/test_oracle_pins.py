@@ -600,3 +600,70 @@ def test_protected_rows_total_order_ties():
     assert got == [2, 3, 4]
     got = M.protected_rows(segs, -1, np.zeros(6, np.uint8), scores, edge=0, tail=0, budget=4 / 6).tolist()
     assert got == [1, 2, 3, 4]        # +0 ranks above -0
+
+
+# ----------------------------------------------------------------------------
+# adaptive MoE fanout (Sec. 2.4, eq:moe)
+# ----------------------------------------------------------------------------
+def test_moe_fanout_hand_cases():
+    # six weights whose shares are 0.5, 0.2, 0.1, 0.1, 0.05, 0.05, among 8 experts;
+    # scaled by 0.37 so that only the normalized shares reach tau
+    base = np.array([0.05, 0.5, 0.1, 0.2, 0.05, 0.1, 0.0, 0.01], np.float32)
+    p = (base * np.float32(0.37))[None, :]
+    expect = {0.10: 3, 0.80: 3, 0.85: 4, 0.93: 5, 0.99: 6, 1.5: 6}
+    for tau, k in expect.items():
+        idx, w, kk = M.moe_fanout(p, tau)
+        assert kk.tolist() == [k], tau
+    assert idx.tolist() == [[1, 3, 2, 5, 0, 4]]          # equal weights: the lower expert first
+    assert np.array_equal(w[0], p[0, idx[0]])             # original weights, not renormalized
+    assert M.moe_fanout(p, 0.65, min_k=1)[2].tolist() == [2]   # 0.5 + 0.2 >= 0.65 > 0.5
+    assert M.moe_fanout(p, 0.45, min_k=1)[2].tolist() == [1]
+
+
+def _moe_rows(seed, n=300, e=64, ties=False):
+    rng = np.random.default_rng(seed)
+    temp = rng.uniform(0.3, 4.0, size=(n, 1))
+    logits = rng.standard_normal((n, e)) * temp
+    p = np.exp(logits - logits.max(axis=1, keepdims=True))
+    p = (p / p.sum(axis=1, keepdims=True)).astype(np.float32)
+    if ties:
+        p = (np.round(p * 64) / 64).astype(np.float32)
+    return p
+
+
+@pytest.mark.parametrize("ties", [False, True])
+def test_moe_fanout_top6_brute_force(ties):
+    p = _moe_rows(1, ties=ties)
+    idx, w, _ = M.moe_fanout(p, 0.9)
+    for r in range(p.shape[0]):
+        ranked = sorted(range(p.shape[1]), key=lambda x: (-float(p[r, x]), x))[:6]
+        assert idx[r].tolist() == ranked
+        assert np.array_equal(w[r], p[r, ranked])
+
+
+def test_moe_fanout_matches_exact_arithmetic_away_from_tau():
+    """fp64 shares decide the same K wherever no cumulative share lies within
+    1e-5 of tau (the float32 decision can only differ at the threshold)."""
+    p = _moe_rows(2, n=500)
+    for tau in (0.5, 0.7, 0.8, 0.9, 0.95):
+        _, w, k32 = M.moe_fanout(p, tau)
+        w64 = w.astype(np.float64)
+        cum = np.cumsum(w64 / w64.sum(axis=1, keepdims=True), axis=1)
+        ok = np.all(np.abs(cum - tau) > 1e-5, axis=1)
+        k64 = np.array([next((k for k in range(3, 7) if cum[r, k - 1] >= tau), 6) for r in range(p.shape[0])])
+        assert ok.sum() > 400
+        assert np.array_equal(k32[ok], k64[ok])
+        assert np.all((k32 >= 3) & (k32 <= 6))
+
+
+def test_moe_fanout_monotone_in_tau_and_extremes():
+    p = _moe_rows(3)
+    ks = [M.moe_fanout(p, t)[2] for t in np.linspace(0.0, 1.0, 21)]
+    for a, b in zip(ks, ks[1:]):
+        assert np.all(b >= a)
+    assert np.all(M.moe_fanout(p, 0.0)[2] == 3)
+    assert np.all(M.moe_fanout(p, 1.01)[2] == 6)
+    # a row of zeros has no shares: the full top-6 is kept
+    z = np.zeros((1, 16), np.float32)
+    idx, w, k = M.moe_fanout(z, 0.5)
+    assert k.tolist() == [6] and idx.tolist() == [[0, 1, 2, 3, 4, 5]]
