@@ -288,6 +288,35 @@ def protected_set(wl, torch, stream, budgets=(0.10, 0.20, 0.25), reps: int = 5, 
     return {"rows": n, "budgets": res, "edge_rows": 128, "tail_rows": 32768, "dirty_rows": n // 100}
 
 
+def moe_fanout_bench(torch, stream, n_rows: int, n_experts: int = 256, tau: float = 0.9, reps: int = 10):
+    """mla_moe_fanout (eq:moe) on seeded router weights for every row of the
+    workload (256 experts, top-6, minimum fanout 3, tau 0.9): median time, the
+    algorithmic HBM rate, and the mean fanout."""
+    from paper_2609_07008_amd import mla
+    from workloads import router_weights
+    p = torch.from_numpy(router_weights(n_rows, n_experts, seed=70080)).cuda()
+    idx = torch.empty((n_rows, 6), dtype=torch.int32, device="cuda")
+    w = torch.empty((n_rows, 6), dtype=torch.float32, device="cuda")
+    k = torch.empty((n_rows,), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((n_experts,), dtype=torch.int32, device="cuda")
+    args = (p, tau, idx, w, k, cnt)
+    mla.moe_fanout(*args, stream=stream)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        mla.moe_fanout(*args, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ms = float(np.median(ts))
+    nbytes = n_rows * n_experts * 4 + n_rows * (6 * 8 + 4) + n_experts * 4
+    return {"rows": n_rows, "experts": n_experts, "tau": tau, "ms": round(ms, 4),
+            "GB_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1), "bytes": nbytes,
+            "mean_fanout": round(float(k.float().mean().item()), 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -398,6 +427,7 @@ def main():
     if not args.no_offline_producer:
         out["offline_producer"] = offline_producer(wl, torch, stream)
     out["protected_set"] = protected_set(wl, torch, stream)
+    out["moe_fanout"] = moe_fanout_bench(torch, stream, wl.n_rows)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
     print(json.dumps(out), flush=True)

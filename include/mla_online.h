@@ -271,6 +271,35 @@ mla_status mla_protected_rows(const mla_segment* segs, int32_t n_segs, const mla
                               int32_t* prot_rows, int32_t* n_prot, void* workspace, size_t ws_bytes,
                               void* stream);
 
+/* ----------------------------------------------------------------------------
+ * mla_moe_fanout -- the adaptive MoE fanout of Sec. 2.4 (eq:moe) for the
+ * reusable middle layers.  For every token row the router's top_k experts are
+ * ranked by weight (IEEE-754 totalOrder, descending; equal weights go to the
+ * lower expert index), and the fanout is
+ *   K = min{k in [min_k, top_k] : sum_{j<=k} p_(j) / sum_{r<=top_k} p_(r) >= tau}
+ * (top_k when no k qualifies, e.g. when the top_k weights sum to 0).  The paper
+ * uses top_k = 6 and min_k = 3; fence layers keep all six (tau > 1).  The
+ * executed experts are the first K of the ranked list and keep their original
+ * weights: the normalization only decides K.  K is decided in float32: the sum
+ * of the top_k weights left to right, each share a correctly rounded division,
+ * the shares accumulated left to right and compared with tau.
+ *
+ *   n_rows, n_experts  N token rows, E routed experts (top_k <= E <= 1024).
+ *   router        [N, E] float device: the router's weights p.
+ *   top_k, min_k  1 <= min_k <= top_k <= 8.
+ *   tau           the fanout threshold (any non-NaN value).
+ *   expert_idx    [N, top_k] int32 device, written: experts by rank.
+ *   expert_w      [N, top_k] float device, written: their weights p.
+ *   fanout        [N] int32 device, written: K.
+ *   expert_count  [E] int32 device or NULL: written with the number of rows
+ *                 that execute each expert (rank < K).
+ * All device arrays 4-byte aligned.  Errors as for mla_online_attend; the
+ * outputs are exact (integer ranks and copies of the inputs).
+ * ------------------------------------------------------------------------- */
+mla_status mla_moe_fanout(int64_t n_rows, int32_t n_experts, const float* router, int32_t top_k, int32_t min_k,
+                          float tau, int32_t* expert_idx, float* expert_w, int32_t* fanout,
+                          int32_t* expert_count, void* stream);
+
 /* Static description of a status code. */
 const char* mla_status_str(mla_status s);
 

@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "common.h"
+#include "moe.h"
 #include "protect.h"
 
 namespace {
@@ -703,6 +704,40 @@ mla_status mla_protected_rows(const mla_segment* segs, int32_t n_segs, const mla
   a.budget = cfg->budget;
   const hipError_t e = mla::launch_protect(a, s);
   if (e != hipSuccess) return hip_fail(e, "protected-row kernels");
+  return MLA_OK;
+}
+
+mla_status mla_moe_fanout(int64_t n_rows, int32_t n_experts, const float* router, int32_t top_k, int32_t min_k,
+                          float tau, int32_t* expert_idx, float* expert_w, int32_t* fanout, int32_t* expert_count,
+                          void* stream) {
+  g_detail.clear();
+  if (n_rows < 0) return fail(MLA_ERR_SHAPE, "n_rows = %lld", (long long)n_rows);
+  if (top_k < 1 || top_k > mla::kMoeMaxTopK)
+    return fail(MLA_ERR_UNSUPPORTED, "top_k = %d; built: 1 .. %d", top_k, mla::kMoeMaxTopK);
+  if (min_k < 1 || min_k > top_k) return fail(MLA_ERR_SHAPE, "min_k = %d outside [1, top_k = %d]", min_k, top_k);
+  if (n_experts < top_k) return fail(MLA_ERR_SHAPE, "n_experts = %d < top_k = %d", n_experts, top_k);
+  if (n_experts > mla::kMoeMaxExperts)
+    return fail(MLA_ERR_UNSUPPORTED, "n_experts = %d; built: up to %d", n_experts, mla::kMoeMaxExperts);
+  if (std::isnan(tau)) return fail(MLA_ERR_SHAPE, "tau is NaN");
+  if (n_rows > INT64_MAX / n_experts) return fail(MLA_ERR_SHAPE, "n_rows * n_experts overflows");
+  if (n_rows > 0 && (router == nullptr || expert_idx == nullptr || expert_w == nullptr || fanout == nullptr))
+    return fail(MLA_ERR_NULL, "router, expert_idx, expert_w and fanout are required");
+  const void* ptrs[] = {router, expert_idx, expert_w, fanout, expert_count};
+  for (const void* q : ptrs)
+    if ((reinterpret_cast<uintptr_t>(q) & 3u) != 0) return fail(MLA_ERR_SHAPE, "arrays must be 4-byte aligned");
+  mla::MoeArgs a{};
+  a.router = router;
+  a.expert_idx = expert_idx;
+  a.expert_w = expert_w;
+  a.fanout = fanout;
+  a.expert_count = expert_count;
+  a.n_rows = n_rows;
+  a.n_experts = n_experts;
+  a.top_k = top_k;
+  a.min_k = min_k;
+  a.tau = tau;
+  const hipError_t e = mla::launch_moe_fanout(a, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "MoE fanout kernel");
   return MLA_OK;
 }
 

@@ -21,7 +21,7 @@ STATUS = {0: "MLA_OK", 1: "MLA_ERR_NULL", 2: "MLA_ERR_SHAPE", 3: "MLA_ERR_UNSUPP
           4: "MLA_ERR_SEGMENTS", 5: "MLA_ERR_ROWS", 6: "MLA_ERR_WORKSPACE", 7: "MLA_ERR_HIP"}
 EXPORTS = ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
            "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query", "mla_protected_rows",
-           "mla_status_str", "mla_last_error_detail", "mla_version")
+           "mla_moe_fanout", "mla_status_str", "mla_last_error_detail", "mla_version")
 
 
 class MlaError(RuntimeError):
@@ -61,9 +61,10 @@ def _load(path: str = LIB_PATH):
     lib.mla_offline_produce.argtypes = [GP, SP, I32, P, P, P, P, I32, P, P, SZ, P]
     lib.mla_protected_rows_query.argtypes = [SP, I32, ctypes.POINTER(SZ)]
     lib.mla_protected_rows.argtypes = [SP, I32, ctypes.POINTER(ProtectCfg), P, P, P, P, P, SZ, P]
+    lib.mla_moe_fanout.argtypes = [I64, I32, P, I32, I32, ctypes.c_float, P, P, P, P, P]
     for f in ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
               "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query",
-              "mla_protected_rows"):
+              "mla_protected_rows", "mla_moe_fanout"):
         getattr(lib, f).restype = ctypes.c_int
     lib.mla_status_str.argtypes = [ctypes.c_int]
     lib.mla_status_str.restype = ctypes.c_char_p
@@ -187,6 +188,16 @@ def protected_rows(segs, query_seg, edge_rows, tail_rows, budget, row_flags, sco
     _check(LIB.mla_protected_rows(sarr, ns, ctypes.byref(cfg), _ptr(row_flags), _ptr(scores), _ptr(prot_rows),
                                   _ptr(n_prot), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                   _stream(stream)))
+
+
+def moe_fanout(router, tau, expert_idx, expert_w, fanout, expert_count=None, top_k: int = 6, min_k: int = 3,
+               stream=None):
+    """Adaptive MoE fanout (mla_moe_fanout) of the device tensor router [N, E]
+    float32 into expert_idx [N, top_k] int32, expert_w [N, top_k] float32,
+    fanout [N] int32 and, if given, expert_count [E] int32."""
+    n, e = (int(router.shape[0]), int(router.shape[1])) if router is not None else (0, 0)
+    _check(LIB.mla_moe_fanout(n, e, _ptr(router), int(top_k), int(min_k), float(tau), _ptr(expert_idx),
+                              _ptr(expert_w), _ptr(fanout), _ptr(expert_count), _stream(stream)))
 
 
 def version() -> str:

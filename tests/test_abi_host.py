@@ -223,3 +223,23 @@ def test_protected_rows_rejects(mla):
     sb, nb = mla.make_segments(bad)
     cfg = mla.ProtectCfg(0, 4, 8, 0.1)
     assert mla.LIB.mla_protected_rows(sb, nb, ctypes.byref(cfg), None, None, P(ok), P(ok), P(ok), ws, None) == 4
+
+
+def test_moe_fanout_rejects():
+    from paper_2609_07008_amd import mla
+    L = mla.LIB
+    P = ctypes.c_void_p
+    fake = P(4096)
+
+    def call(n=4, e=16, router=fake, top_k=6, min_k=3, tau=0.9, idx=fake, w=fake, k=fake, cnt=None):
+        return L.mla_moe_fanout(n, e, router, top_k, min_k, tau, idx, w, k, cnt, None)
+
+    assert call(n=-1) == 2
+    assert call(top_k=0) == 3 and call(top_k=9) == 3
+    assert call(min_k=0) == 2 and call(min_k=7) == 2
+    assert call(e=5) == 2
+    assert call(e=1025) == 3
+    assert call(tau=float("nan")) == 2
+    assert call(router=None) == 1 and call(idx=None) == 1 and call(w=None) == 1 and call(k=None) == 1
+    assert call(w=P(4098)) == 2
+    assert call(n=2**62, e=16) == 2
