@@ -38,6 +38,9 @@ What it computes, and where the paper defines it:
   query rows, new and dirty rows, the first and last rows of every relocated
   segment, the recent tail, and the Indexer's top rows, which top the
   protected share of the candidate rows up to the controller's budget.
+* ``shared_wb`` -- the shared second projection y = W_b z (Sec. 2.1
+  eq:factorization; Alg. 2 returns W_b z), with W_b stored as a linear
+  layer's weight [d_out, d_in].
 * ``moe_fanout`` -- the adaptive MoE fanout of Sec. 2.4 (eq:moe): per token
   row, the router's top-6 experts, and the smallest fanout K in {3,..,6} whose
   normalized top-6 weights reach tau; executed experts keep their original
@@ -470,3 +473,11 @@ def moe_fanout(router, tau: float, top_k: int = 6, min_k: int = 3):
                 k_out[hit] = j + 1
                 decided |= hit
     return idx, w, k_out
+
+
+# ----------------------------------------------------------------------------
+# shared second projection (Sec. 2.1 eq:factorization, Alg. 2)
+# ----------------------------------------------------------------------------
+def shared_wb(z, w_b) -> np.ndarray:
+    """y = W_b z for every row: y[r, o] = sum_i w_b[o, i] z[r, i], in fp64."""
+    return np.asarray(z, dtype=F64) @ np.asarray(w_b, dtype=F64).T

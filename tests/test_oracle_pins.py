@@ -667,3 +667,21 @@ def test_moe_fanout_monotone_in_tau_and_extremes():
     z = np.zeros((1, 16), np.float32)
     idx, w, k = M.moe_fanout(z, 0.5)
     assert k.tolist() == [6] and idx.tolist() == [[0, 1, 2, 3, 4, 5]]
+
+
+# ----------------------------------------------------------------------------
+# shared second projection y = W_b z (Sec. 2.1 eq:factorization, Alg. 2)
+# ----------------------------------------------------------------------------
+def test_shared_wb_brute_force_and_identities():
+    rng = np.random.default_rng(4)
+    z = rng.standard_normal((5, 7))
+    w = rng.standard_normal((3, 7))           # [d_out, d_in], not square: a transposed operand fails
+    y = M.shared_wb(z, w)
+    assert y.shape == (5, 3)
+    for r in range(5):
+        for o in range(3):
+            assert abs(y[r, o] - sum(w[o, i] * z[r, i] for i in range(7))) < 1e-12
+    assert np.allclose(M.shared_wb(z, np.eye(7)), z, rtol=0, atol=1e-15)
+    # y = W_b (z_off + z_online) = W_b z_off + W_b z_online (eq:factorization meets one W_b)
+    z2 = rng.standard_normal((5, 7))
+    assert np.allclose(M.shared_wb(z + z2, w), M.shared_wb(z, w) + M.shared_wb(z2, w), rtol=0, atol=1e-12)
