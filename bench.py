@@ -317,6 +317,33 @@ def moe_fanout_bench(torch, stream, n_rows: int, n_experts: int = 256, tau: floa
             "mean_fanout": round(float(k.float().mean().item()), 4)}
 
 
+def shared_wb_bench(torch, stream, n_rows: int, d: int = 4096, reps: int = 5):
+    """mla_shared_wb: y = W_b z over every row of the workload (z [N, 4096] bf16
+    drawn on the device, W_b [4096, 4096] bf16 with std 0.02, y fp32): median time
+    and the MFMA rate against the dense bf16 peak."""
+    from paper_2609_07008_amd import mla
+    g = torch.Generator(device="cuda")
+    g.manual_seed(70082)
+    z = (torch.randn((n_rows, d), generator=g, device="cuda") * 0.05).to(torch.bfloat16)
+    w = (torch.randn((d, d), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    y = torch.empty((n_rows, d), dtype=torch.float32, device="cuda")
+    mla.shared_wb(z, w, y, stream=stream)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        mla.shared_wb(z, w, y, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ms = float(np.median(ts))
+    flop = 2.0 * n_rows * d * d
+    del z, w, y
+    return {"rows": n_rows, "d_in": d, "d_out": d, "ms": round(ms, 3), "flop": flop,
+            "TFLOP_per_s": round(flop / (ms * 1e-3) / 1e12, 1), "frac_of_bf16_peak": round(flop / (ms * 1e-3) / 2.5e15, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -428,6 +455,7 @@ def main():
         out["offline_producer"] = offline_producer(wl, torch, stream)
     out["protected_set"] = protected_set(wl, torch, stream)
     out["moe_fanout"] = moe_fanout_bench(torch, stream, wl.n_rows)
+    out["shared_wb"] = shared_wb_bench(torch, stream, wl.n_rows)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -15,7 +15,9 @@
  *   4. the group-aligned sliced first output projection W_a, with the offline
  *      Local-head artifact z_off added on unprotected rows and replaced (never
  *      added) on protected rows (RestoreAndReplace, eq:factorization).
- * The shared second projection W_b is outside this library.
+ * Beside the step the library exports the offline producer of the artifact
+ * (Alg. 1), the protected token-row set (eq:protected), the shared second
+ * projection y = W_b z and the adaptive MoE fanout (eq:moe).
  *
  * Conventions (all entry points):
  *  - Host arrays are read during the call only.  Device arrays are owned by the
@@ -299,6 +301,23 @@ mla_status mla_protected_rows(const mla_segment* segs, int32_t n_segs, const mla
 mla_status mla_moe_fanout(int64_t n_rows, int32_t n_experts, const float* router, int32_t top_k, int32_t min_k,
                           float tau, int32_t* expert_idx, float* expert_w, int32_t* fanout,
                           int32_t* expert_count, void* stream);
+
+/* ----------------------------------------------------------------------------
+ * mla_shared_wb -- the shared second output projection y = W_b z that every row's
+ * group-sliced state z meets after the artifact add (Sec. 2.1 eq:factorization,
+ * Alg. 2 returns W_b z).  bf16 MFMA with fp32 accumulation.
+ *
+ *   n_rows, d_in, d_out  N rows; z width (a multiple of 64, at most 16384);
+ *                  output channels (>= 1).
+ *   z              [N, d_in] bf16 device (the state z, in bf16).
+ *   w_b            [d_out, d_in] bf16 device (a linear layer's weight: row o holds
+ *                  the d_in weights of output channel o).
+ *   out_dtype      MLA_BF16 or MLA_F32 for y.
+ *   y              [N, d_out] device, written.
+ * Device arrays 16-byte aligned.  Errors as for mla_online_attend.
+ * ------------------------------------------------------------------------- */
+mla_status mla_shared_wb(int64_t n_rows, int32_t d_in, int32_t d_out, const void* z, const void* w_b,
+                         int32_t out_dtype, void* y, void* stream);
 
 /* Static description of a status code. */
 const char* mla_status_str(mla_status s);

@@ -15,6 +15,7 @@
 #include "common.h"
 #include "moe.h"
 #include "protect.h"
+#include "wb.h"
 
 namespace {
 
@@ -738,6 +739,32 @@ mla_status mla_moe_fanout(int64_t n_rows, int32_t n_experts, const float* router
   a.tau = tau;
   const hipError_t e = mla::launch_moe_fanout(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "MoE fanout kernel");
+  return MLA_OK;
+}
+
+mla_status mla_shared_wb(int64_t n_rows, int32_t d_in, int32_t d_out, const void* z, const void* w_b,
+                         int32_t out_dtype, void* y, void* stream) {
+  g_detail.clear();
+  if (n_rows < 0) return fail(MLA_ERR_SHAPE, "n_rows = %lld", (long long)n_rows);
+  if (d_in < 64 || d_in % 64 != 0) return fail(MLA_ERR_SHAPE, "d_in = %d must be a positive multiple of 64", d_in);
+  if (d_in > mla::kWbMaxDin) return fail(MLA_ERR_UNSUPPORTED, "d_in = %d; built: up to %d", d_in, mla::kWbMaxDin);
+  if (d_out < 1) return fail(MLA_ERR_SHAPE, "d_out = %d", d_out);
+  if (out_dtype != MLA_BF16 && out_dtype != MLA_F32) return fail(MLA_ERR_SHAPE, "out_dtype %d", out_dtype);
+  if ((n_rows + 255) / 256 * ((d_out + 255) / 256) > (int64_t)INT32_MAX - 8)
+    return fail(MLA_ERR_UNSUPPORTED, "n_rows = %lld: too many tiles", (long long)n_rows);
+  if (n_rows == 0) return MLA_OK;
+  if (z == nullptr || w_b == nullptr || y == nullptr) return fail(MLA_ERR_NULL, "z, w_b and y are required");
+  if (!aligned16(z) || !aligned16(w_b) || !aligned16(y)) return fail(MLA_ERR_SHAPE, "z, w_b and y must be 16-byte aligned");
+  mla::WbArgs a{};
+  a.z = reinterpret_cast<const uint16_t*>(z);
+  a.w_b = reinterpret_cast<const uint16_t*>(w_b);
+  a.y = y;
+  a.n_rows = n_rows;
+  a.d_in = d_in;
+  a.d_out = d_out;
+  a.y_bf16 = out_dtype == MLA_BF16 ? 1 : 0;
+  const hipError_t e = mla::launch_wb(a, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "shared W_b kernel");
   return MLA_OK;
 }
 

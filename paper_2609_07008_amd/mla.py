@@ -21,7 +21,7 @@ STATUS = {0: "MLA_OK", 1: "MLA_ERR_NULL", 2: "MLA_ERR_SHAPE", 3: "MLA_ERR_UNSUPP
           4: "MLA_ERR_SEGMENTS", 5: "MLA_ERR_ROWS", 6: "MLA_ERR_WORKSPACE", 7: "MLA_ERR_HIP"}
 EXPORTS = ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
            "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query", "mla_protected_rows",
-           "mla_moe_fanout", "mla_status_str", "mla_last_error_detail", "mla_version")
+           "mla_moe_fanout", "mla_shared_wb", "mla_status_str", "mla_last_error_detail", "mla_version")
 
 
 class MlaError(RuntimeError):
@@ -62,9 +62,10 @@ def _load(path: str = LIB_PATH):
     lib.mla_protected_rows_query.argtypes = [SP, I32, ctypes.POINTER(SZ)]
     lib.mla_protected_rows.argtypes = [SP, I32, ctypes.POINTER(ProtectCfg), P, P, P, P, P, SZ, P]
     lib.mla_moe_fanout.argtypes = [I64, I32, P, I32, I32, ctypes.c_float, P, P, P, P, P]
+    lib.mla_shared_wb.argtypes = [I64, I32, I32, P, P, I32, P, P]
     for f in ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
               "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query",
-              "mla_protected_rows", "mla_moe_fanout"):
+              "mla_protected_rows", "mla_moe_fanout", "mla_shared_wb"):
         getattr(lib, f).restype = ctypes.c_int
     lib.mla_status_str.argtypes = [ctypes.c_int]
     lib.mla_status_str.restype = ctypes.c_char_p
@@ -198,6 +199,15 @@ def moe_fanout(router, tau, expert_idx, expert_w, fanout, expert_count=None, top
     n, e = (int(router.shape[0]), int(router.shape[1])) if router is not None else (0, 0)
     _check(LIB.mla_moe_fanout(n, e, _ptr(router), int(top_k), int(min_k), float(tau), _ptr(expert_idx),
                               _ptr(expert_w), _ptr(fanout), _ptr(expert_count), _stream(stream)))
+
+
+def shared_wb(z, w_b, y, stream=None):
+    """y = W_b z (mla_shared_wb): z [N, d_in] bf16 and w_b [d_out, d_in] bf16 device
+    tensors, y [N, d_out] float32 or bfloat16."""
+    n, d_in = int(z.shape[0]), int(z.shape[1])
+    d_out = int(w_b.shape[0])
+    out = MLA_BF16 if y.dtype == torch.bfloat16 else MLA_F32
+    _check(LIB.mla_shared_wb(n, d_in, d_out, _ptr(z), _ptr(w_b), out, _ptr(y), _stream(stream)))
 
 
 def version() -> str:

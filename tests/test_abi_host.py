@@ -243,3 +243,22 @@ def test_moe_fanout_rejects():
     assert call(router=None) == 1 and call(idx=None) == 1 and call(w=None) == 1 and call(k=None) == 1
     assert call(w=P(4098)) == 2
     assert call(n=2**62, e=16) == 2
+
+
+def test_shared_wb_rejects():
+    from paper_2609_07008_amd import mla
+    L = mla.LIB
+    P = ctypes.c_void_p
+    fake = P(4096)
+
+    def call(n=4, d_in=64, d_out=16, z=fake, w=fake, out=1, y=fake):
+        return L.mla_shared_wb(n, d_in, d_out, z, w, out, y, None)
+
+    assert call(n=-1) == 2
+    assert call(d_in=0) == 2 and call(d_in=96) == 2 and call(d_in=32) == 2
+    assert call(d_in=16448) == 3
+    assert call(d_out=0) == 2
+    assert call(out=5) == 2
+    assert call(z=None) == 1 and call(w=None) == 1 and call(y=None) == 1
+    assert call(z=P(4104)) == 2
+    assert call(n=0, z=None) == 0
