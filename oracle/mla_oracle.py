@@ -49,7 +49,12 @@ What it computes, and where the paper defines it:
   as the GPU kernel decides it.
 
 Readings where the paper is silent: V is the latent itself, so the inverse
-output RoPE and RestorePhase are the identity; a key is visible to a row iff
+output RoPE and RestorePhase are the identity -- unless the geometry's
+``value_rope`` is set: then the value is the whole latent row [c ; k_r] at the
+key's true position, a head output's RoPE part is rotated back by the query's
+position (R^{-1}, eq:offonline), and the factorized route restores each
+canonical-frame partial's phase by R(+p_s) before the merge (RestorePhase,
+Alg. 2); a key is visible to a row iff
 its true position is <= the row's (the diagonal included); every request row is
 an output row, Global heads run on every row and Local heads only on protected
 rows (Alg. 2 writes O_G without and O_{L,A} with the protected-set subscript).
@@ -137,24 +142,32 @@ class TrueKeys:
         self.base = base
 
 
-def attend_direct(keys: TrueKeys, q: np.ndarray, t: int, scale: float):
+def attend_direct(keys: TrueKeys, q: np.ndarray, t: int, scale: float, value_rope: bool = False):
     """Unfactorized attention of one row at true position t.  q [nh, d_c + d_r]
     holds absorbed queries with the RoPE part not yet rotated; it is rotated
-    to position t and scored against every key at true position <= t."""
+    to position t and scored against every key at true position <= t.
+    value_rope: the values are the true-position key rows [c ; R(P) k^] and the
+    output's RoPE part is rotated back by R(-t) (inverse output RoPE)."""
     q = np.asarray(q, dtype=F64)
     d_c = keys.d_latent
     qt = np.concatenate([q[:, :d_c], rope(q[:, d_c:], np.full(q.shape[0], t), keys.base)], axis=1)
     vis = keys.k[: t + 1]
     scores = F64(scale) * (qt @ vis.T)
-    return softmax_stats(scores, keys.c[: t + 1])
+    if not value_rope:
+        return softmax_stats(scores, keys.c[: t + 1])
+    o, lse = softmax_stats(scores, vis)
+    o[:, d_c:] = rope(o[:, d_c:], np.full(o.shape[0], -t), keys.base)
+    return o, lse
 
 
 def attend_segment(kv: np.ndarray, seg_row: np.ndarray, q: np.ndarray, delta: int,
-                   scale: float, d_latent: int, base: float):
+                   scale: float, d_latent: int, base: float, value_rope: bool = False):
     """One segment of the factorized route: the query is relocated into the
     segment's canonical frame by R(delta) with delta = t - p_s (eq:rope), and
     scored against the canonical keys of the segment at offsets u <= delta.
-    Returns (o_s, lse_s) or None when the segment is not visible."""
+    Returns (o_s, lse_s) or None when the segment is not visible.  value_rope:
+    the values are the canonical latent rows [c ; k_r], so o_s is in the
+    segment's canonical frame (its phase is restored by the caller)."""
     ks, ln, _ = seg_row
     lim = min(delta, ln - 1)
     if lim < 0:
@@ -163,7 +176,7 @@ def attend_segment(kv: np.ndarray, seg_row: np.ndarray, q: np.ndarray, delta: in
     kc = np.asarray(kv[ks:ks + lim + 1], dtype=F64)
     qd = np.concatenate([q[:, :d_latent], rope(q[:, d_latent:], np.full(q.shape[0], delta), base)], axis=1)
     scores = F64(scale) * (qd @ kc.T)
-    return softmax_stats(scores, kc[:, :d_latent])
+    return softmax_stats(scores, kc if value_rope else kc[:, :d_latent])
 
 
 def lse_merge(o: np.ndarray, lse: np.ndarray):
@@ -178,27 +191,38 @@ def lse_merge(o: np.ndarray, lse: np.ndarray):
     return out, m + np.log(wsum)
 
 
-def attend_factorized(kv, segs, q, t, scale, d_latent, base):
+def attend_factorized(kv, segs, q, t, scale, d_latent, base, value_rope: bool = False, restore: bool = True):
     """Alg. 2 for one row: relocate per visible segment (request order), attend
-    to the canonical latent of that segment, then merge the partials."""
+    to the canonical latent of that segment, then merge the partials.
+    value_rope: each partial's RoPE part is moved from the segment's canonical
+    frame to true positions by R(+p_s) (RestorePhase; `restore=False` skips it,
+    for the tests), and after the merge rotated back by R(-t) (R^{-1})."""
     segs = np.asarray(segs, dtype=np.int64)
     parts_o, parts_l = [], []
     for s in np.argsort(segs[:, 2], kind="stable"):
         delta = int(t - segs[s, 2])
-        r = attend_segment(kv, segs[s], q, delta, scale, d_latent, base)
+        r = attend_segment(kv, segs[s], q, delta, scale, d_latent, base, value_rope)
         if r is not None:
-            parts_o.append(r[0])
+            o_s = r[0]
+            if value_rope and restore:
+                o_s = o_s.copy()
+                o_s[:, d_latent:] = rope(o_s[:, d_latent:], np.full(o_s.shape[0], int(segs[s, 2])), base)
+            parts_o.append(o_s)
             parts_l.append(r[1])
-    return lse_merge(np.stack(parts_o), np.stack(parts_l))
+    o, lse = lse_merge(np.stack(parts_o), np.stack(parts_l))
+    if value_rope:
+        o[:, d_latent:] = rope(o[:, d_latent:], np.full(o.shape[0], -int(t)), base)
+    return o, lse
 
 
 # ----------------------------------------------------------------------------
 # first output projection (Sec. 2.1 eq:offonline, Alg. 2)
 # ----------------------------------------------------------------------------
 def dense_blocks(w_o: np.ndarray, n_heads: int, d_latent: int, d_model: int) -> np.ndarray:
-    """Expand W_o [n_pg, (H/n_pg)*d_c, d_model/n_pg] into per-head blocks
-    [H, d_c, d_model]: head h of projection group pg = h // (H/n_pg) maps its
-    d_c outputs to channels pg*d_model/n_pg .. (pg+1)*d_model/n_pg, zero elsewhere."""
+    """Expand W_o [n_pg, (H/n_pg)*d_v, d_model/n_pg] into per-head blocks
+    [H, d_v, d_model] (d_v = the head output width, passed as `d_latent`): head h
+    of projection group pg = h // (H/n_pg) maps its d_v outputs to channels
+    pg*d_model/n_pg .. (pg+1)*d_model/n_pg, zero elsewhere."""
     w_o = np.asarray(w_o, dtype=F64)
     npg = w_o.shape[0]
     hp = n_heads // npg
@@ -242,7 +266,9 @@ def reference_rows(wl, rows, z_off=None, kv=None, keys=None, w_o=None, exact=Fal
         keys = TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
     if w_o is None:
         w_o = wl.w_o(exact=exact)
-    blocks = dense_blocks(w_o, g.n_heads, g.d_latent, g.d_model)
+    vr = bool(getattr(g, "value_rope", False))
+    dv = g.d_latent + (g.d_rope if vr else 0)
+    blocks = dense_blocks(w_o, g.n_heads, dv, g.d_model)
     glob_ids = wl.global_head_ids()
     loc_ids = wl.local_head_ids()
     prot = np.asarray(wl.prot_rows, dtype=np.int64)
@@ -252,7 +278,7 @@ def reference_rows(wl, rows, z_off=None, kv=None, keys=None, w_o=None, exact=Fal
     ql = wl.q_loc(idx=pidx, exact=exact) if pidx else None
     res = RowResult()
     res.rows = rows
-    res.o_glob = np.zeros((rows.shape[0], g.n_groups, g.d_latent))
+    res.o_glob = np.zeros((rows.shape[0], g.n_groups, dv))
     res.lse_glob = np.zeros((rows.shape[0], g.n_groups))
     res.o_loc, res.lse_loc, res.prot_idx = {}, {}, {}
     res.z_online = np.zeros((rows.shape[0], g.d_model))
@@ -260,15 +286,15 @@ def reference_rows(wl, rows, z_off=None, kv=None, keys=None, w_o=None, exact=Fal
     k = 0
     for i, r in enumerate(rows):
         t = int(pos[r])
-        o, lse = attend_direct(keys, qg[i], t, g.softmax_scale)
+        o, lse = attend_direct(keys, qg[i], t, g.softmax_scale, vr)
         res.o_glob[i], res.lse_glob[i] = o, lse
         zon = project(o, glob_ids, blocks)
         if int(r) in prot_index:
             q = ql[k].reshape(-1, g.d_qk)
             k += 1
-            ol, ll = attend_direct(keys, q, t, g.softmax_scale)
+            ol, ll = attend_direct(keys, q, t, g.softmax_scale, vr)
             hl = g.heads_per_group - 1
-            res.o_loc[i] = ol.reshape(g.n_groups, hl, g.d_latent)
+            res.o_loc[i] = ol.reshape(g.n_groups, hl, dv)
             res.lse_loc[i] = ll.reshape(g.n_groups, hl)
             res.prot_idx[i] = prot_index[int(r)]
             zon = zon + project(ol, loc_ids.reshape(-1), blocks)
@@ -291,13 +317,15 @@ def full_recompute_rows(wl, rows, kv=None, w_o=None, exact=True, q_all=None):
     keys = TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
     if w_o is None:
         w_o = wl.w_o(exact=exact)
-    blocks = dense_blocks(w_o, g.n_heads, g.d_latent, g.d_model)
+    vr = bool(getattr(g, "value_rope", False))
+    dv = g.d_latent + (g.d_rope if vr else 0)
+    blocks = dense_blocks(w_o, g.n_heads, dv, g.d_model)
     if q_all is None:
         q_all = wl.q_full(exact=exact)
-    out_o = np.zeros((rows.shape[0], g.n_heads, g.d_latent))
+    out_o = np.zeros((rows.shape[0], g.n_heads, dv))
     z = np.zeros((rows.shape[0], g.d_model))
     for i, r in enumerate(rows):
-        o, _ = attend_direct(keys, q_all[r], int(pos[r]), g.softmax_scale)
+        o, _ = attend_direct(keys, q_all[r], int(pos[r]), g.softmax_scale, vr)
         out_o[i] = o
         z[i] = project(o, range(g.n_heads), blocks)
     return out_o, z
@@ -316,7 +344,9 @@ def artifact(wl, kv=None, q_all=None, w_o=None, exact=False) -> np.ndarray:
         q_all = wl.q_full(exact=exact)
     if w_o is None:
         w_o = wl.w_o(exact=exact)
-    blocks = dense_blocks(w_o, g.n_heads, g.d_latent, g.d_model)
+    vr = bool(getattr(g, "value_rope", False))
+    dv = g.d_latent + (g.d_rope if vr else 0)
+    blocks = dense_blocks(w_o, g.n_heads, dv, g.d_model)
     loc = wl.local_head_ids().reshape(-1)
     z_off = np.zeros((wl.n_rows, g.d_model))
     for ks, ln, _ in np.asarray(wl.segs):
@@ -325,7 +355,9 @@ def artifact(wl, kv=None, q_all=None, w_o=None, exact=False) -> np.ndarray:
             q = np.asarray(q_all[ks + u][loc], dtype=F64)
             qc = np.concatenate([q[:, :g.d_latent], rope(q[:, g.d_latent:], np.full(q.shape[0], u), g.rope_base)], axis=1)
             scores = F64(g.softmax_scale) * (qc @ kc[: u + 1].T)
-            o, _ = softmax_stats(scores, kc[: u + 1, :g.d_latent])
+            o, _ = softmax_stats(scores, kc[: u + 1, :dv])
+            if vr:   # canonical values carry R(u'); R^{-1} at the row's canonical position u
+                o[:, g.d_latent:] = rope(o[:, g.d_latent:], np.full(o.shape[0], -u), g.rope_base)
             z_off[ks + u] = project(o, loc, blocks)
     return z_off
 

@@ -685,3 +685,76 @@ def test_shared_wb_brute_force_and_identities():
     # y = W_b (z_off + z_online) = W_b z_off + W_b z_online (eq:factorization meets one W_b)
     z2 = rng.standard_normal((5, 7))
     assert np.allclose(M.shared_wb(z + z2, w), M.shared_wb(z, w) + M.shared_wb(z2, w), rtol=0, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# rotary value: RestorePhase per segment and inverse output RoPE (Sec. 2.1
+# eq:offonline, Alg. 2)
+# ----------------------------------------------------------------------------
+def _vrope_family(seed):
+    rng = np.random.default_rng(500 + seed)
+    nd = int(rng.integers(2, 5))
+    lens = [int(x) for x in rng.integers(1, 30, size=nd)]
+    perm = [int(x) for x in rng.permutation(nd)]
+    return make_custom(lens, req_perm=perm, tq=int(rng.integers(1, 6)), H=4, G=2, d_c=16, d_r=8,
+                       d_model=8, prot_frac=0.3, seed=600 + seed, value_rope=True)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_value_rope_factorized_equals_direct(seed):
+    """With a rotary value the factorized route equals the direct definition
+    only when each partial's phase is restored (R(+p_s)) before the merge: the
+    restore is what the GPU must reproduce, and dropping it is caught here."""
+    wl = _vrope_family(seed)
+    g = wl.geom
+    kv = wl.kv(exact=True)
+    q = wl.q_full(exact=True)
+    keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    _, _, pos = M.row_geometry(wl.segs)
+    worst, worst_unrestored = 0.0, 0.0
+    for r in range(wl.n_rows):
+        od, ld = M.attend_direct(keys, q[r], int(pos[r]), g.softmax_scale, value_rope=True)
+        of, lf = M.attend_factorized(kv, wl.segs, q[r], int(pos[r]), g.softmax_scale, g.d_latent,
+                                     g.rope_base, value_rope=True)
+        ou, _ = M.attend_factorized(kv, wl.segs, q[r], int(pos[r]), g.softmax_scale, g.d_latent,
+                                    g.rope_base, value_rope=True, restore=False)
+        assert od.shape[1] == g.d_latent + g.d_rope
+        assert np.allclose(od[:, :g.d_latent], M.attend_direct(keys, q[r], int(pos[r]), g.softmax_scale)[0],
+                           rtol=0, atol=1e-14)                      # the latent part is unchanged
+        worst = max(worst, rel(of, od), np.abs(lf - ld).max() / (1 + np.abs(ld).max()))
+        worst_unrestored = max(worst_unrestored, rel(ou, od))
+    assert worst < 1e-11, worst
+    assert worst_unrestored > 1e-3
+
+
+def test_value_rope_relative_rotation_brute_force():
+    """The head output's RoPE part is sum_j softmax_j R(P_j - t) k^_j: each
+    value rotated by its position relative to the query (R^{-1} R(P) = R(P - t)),
+    written here key by key from the raw keys k^ = R(-u) k_r."""
+    wl = _vrope_family(1)
+    g = wl.geom
+    kv = wl.kv(exact=True)
+    q = wl.q_full(exact=True)
+    keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    seg, u, pos = M.row_geometry(wl.segs)
+    by_pos = np.argsort(pos)
+    for r in range(0, wl.n_rows, 3):
+        t = int(pos[r])
+        od, _ = M.attend_direct(keys, q[r], t, g.softmax_scale, value_rope=True)
+        qt = np.concatenate([q[r][:, :g.d_latent], M.rope(q[r][:, g.d_latent:], np.full(g.n_heads, t), g.rope_base)],
+                            axis=1)
+        s = g.softmax_scale * (qt @ keys.k[: t + 1].T)
+        w = np.exp(s - s.max(axis=1, keepdims=True))
+        w /= w.sum(axis=1, keepdims=True)
+        acc = np.zeros((g.n_heads, g.d_rope))
+        for p_j in range(t + 1):
+            j = by_pos[p_j]
+            raw = M.rope(kv[j:j + 1, g.d_latent:].astype(np.float64), np.array([-u[j]]), g.rope_base)[0]
+            acc += w[:, p_j:p_j + 1] * M.rope(raw[None, :], np.array([p_j - t]), g.rope_base)[0][None, :]
+        assert rel(od[:, g.d_latent:], acc) < 1e-12
+
+
+def test_value_rope_prefix_document_artifact_is_exact():
+    wl = make_custom([10, 13, 8], req_perm=[1, 0, 2], tq=4, H=4, G=2, d_c=16, d_r=4, d_model=8,
+                     seed=8, prot_frac=0.25, value_rope=True)
+    check_prefix_document(wl)

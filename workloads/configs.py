@@ -67,6 +67,12 @@ class Geometry:
     n_proj_groups: int    # 1 = dense first projection; G = group-sliced
     softmax_scale: float
     rope_base: float = 10000.0
+    value_rope: bool = False  # the value is the whole latent row (its RoPE part rotary)
+
+    @property
+    def d_v(self) -> int:
+        """Width of a head output: d_c, or d_c + d_r when the value carries the RoPE part."""
+        return self.d_latent + (self.d_rope if self.value_rope else 0)
 
     @property
     def heads_per_group(self) -> int:
@@ -199,11 +205,11 @@ class Workload:
         return self._draw_rows(_T_QL, self.n_prot, parts, idx, not exact, threads)
 
     def w_o(self, exact=False) -> np.ndarray:
-        """First output projection [n_pg, (H/n_pg)*d_c, d_model/n_pg]; block pg maps the
-        latent outputs of heads pg*H/n_pg .. to channels pg*d_model/n_pg .."""
+        """First output projection [n_pg, (H/n_pg)*d_v, d_model/n_pg]; block pg maps the
+        head outputs of heads pg*H/n_pg .. to channels pg*d_model/n_pg .."""
         g = self.geom
         npg = g.n_proj_groups
-        rows = (g.n_heads // npg) * g.d_latent
+        rows = (g.n_heads // npg) * g.d_v
         cols = g.d_model // npg
         x = self._rng(_T_WO, 0).standard_normal((npg, rows, cols), dtype=np.float32)
         x *= np.float32(self.std["wo"])
@@ -355,7 +361,8 @@ def make_workload(cfg: int, variant: str = "default", seed: int | None = None,
 
 
 def make_custom(doc_lens, req_perm=None, tq=8, H=4, G=2, d_c=64, d_r=16, d_model=32, n_pg=None,
-                prot_frac=0.2, seed=1234, glob_head=None, fp32=True, std=None, prot_rows=None):
+                prot_frac=0.2, seed=1234, glob_head=None, fp32=True, std=None, prot_rows=None,
+                value_rope=False):
     """Small workload family for exactness tests: arbitrary document lengths, optional
     request-order permutation, arbitrary head partition."""
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, _T_STRUCT, 1])))
@@ -386,7 +393,7 @@ def make_custom(doc_lens, req_perm=None, tq=8, H=4, G=2, d_c=64, d_r=16, d_model
         glob_head = rng.integers(0, hpg, size=G)
     if std is None:
         std = dict(c=1.0, kr=1.0, qc=1 / math.sqrt(d_c), qr=1 / math.sqrt(d_r), wo=0.02, zoff=0.05)
-    geom = Geometry(H, G, d_c, d_r, d_model, n_pg or G, 1 / math.sqrt(d_c + d_r))
+    geom = Geometry(H, G, d_c, d_r, d_model, n_pg or G, 1 / math.sqrt(d_c + d_r), value_rope=bool(value_rope))
     return Workload(name="custom", seed=seed, geom=geom, segs=segs,
                     glob_head=np.asarray(glob_head, dtype=np.int32), prot_rows=prot_rows, std=std,
                     fp32_source=fp32, random_zoff=True, query_rows=tq, meta=dict(cfg=0))
