@@ -344,6 +344,54 @@ def shared_wb_bench(torch, stream, n_rows: int, d: int = 4096, reps: int = 5):
             "TFLOP_per_s": round(flop / (ms * 1e-3) / 1e12, 1), "frac_of_bf16_peak": round(flop / (ms * 1e-3) / 2.5e15, 4)}
 
 
+def rotary_value_step(wl, dev, torch, stream, split: int, reps: int = 2):
+    """The step with a rotary value (the value is the whole latent row; each
+    segment's RoPE output dims restored and rotated back by R(-(t - p_s))) on the
+    same resident inputs, with a W_o of d_c + d_r rows per head (bf16, std 0.02,
+    drawn on the device).  Work counted as the method's: 2*576 + 2*576 flop per
+    visible key and head-row, plus the o-proj over 576-wide head outputs."""
+    from dataclasses import replace
+    from paper_2609_07008_amd import mla, step
+    g = replace(wl.geom, value_rope=True)
+    dv = g.d_latent + g.d_rope
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(70083)
+    hp = g.n_heads // g.n_proj_groups
+    w_o = (torch.randn((g.n_proj_groups, hp * dv, g.d_model // g.n_proj_groups), generator=gen, device="cuda")
+           * 0.02).to(torch.bfloat16)
+    st = step.OnlineStep(g, wl.segs, wl.prot_rows, wl.glob_head, split, with_part_seg=False)
+    st.run(dev["kv"], dev["q_glob"], dev["q_loc"], w_o, dev["z_off"])
+    torch.cuda.synchronize()
+    t = []
+    for _ in range(reps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record(stream)
+        st.attend(dev["kv"], dev["q_glob"], dev["q_loc"])
+        e[1].record(stream)
+        st.merge()
+        e[2].record(stream)
+        st.oproj(w_o, dev["z_off"])
+        e[3].record(stream)
+        torch.cuda.synchronize()
+        t.append([e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3]), e[0].elapsed_time(e[3])])
+    t = np.median(np.asarray(t), axis=0)
+    pos = wl.row_position()
+    prot = np.asarray(wl.prot_rows, dtype=np.int64)
+    vis = float((pos + 1).sum()) * g.n_groups + float((pos[prot] + 1).sum()) * g.n_local
+    flop_attn = vis * (2.0 * (g.d_latent + g.d_rope) + 2.0 * dv)
+    head_rows = wl.n_rows * g.n_groups + len(prot) * g.n_local
+    flop_oproj = head_rows * 2.0 * dv * g.d_model / g.n_proj_groups
+    ms = float(t[3])
+    out = {"ms": {"attend": round(float(t[0]), 3), "merge": round(float(t[1]), 3), "oproj": round(float(t[2]), 3),
+                  "step": round(ms, 3)},
+           "flop": flop_attn + flop_oproj,
+           "TFLOP_per_s": round((flop_attn + flop_oproj) / (ms * 1e-3) / 1e12, 1),
+           "pct_bf16_peak": round(100 * (flop_attn + flop_oproj) / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+           "head_output_width": dv}
+    del st, w_o
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -355,6 +403,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-merge-per-segment", action="store_true",
                     help="skip the standalone merge of per-segment partials of the query rows")
+    ap.add_argument("--no-rotary-value", action="store_true",
+                    help="skip the rotary-value step measurement")
     ap.add_argument("--no-offline-producer", action="store_true",
                     help="skip the MLA-Off producer measurement on the same geometry")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
@@ -447,7 +497,11 @@ def main():
                      "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4), "traffic": profiled_traffic(),
                      "kernel": "attend_kernel<512,64> (timed with the plan kernels of mla_online_attend)"},
     }
-    del st, dev
+    del st
+    torch.cuda.empty_cache()
+    if not args.no_rotary_value:
+        out["rotary_value"] = rotary_value_step(wl, dev, torch, stream, split)
+    del dev
     torch.cuda.empty_cache()
     if not args.no_merge_per_segment:
         out["merge_per_segment"] = merge_per_segment(wl, torch, stream)

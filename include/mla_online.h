@@ -66,7 +66,7 @@ typedef enum mla_dtype { MLA_BF16 = 0, MLA_F32 = 1 } mla_dtype;
 /* Layer geometry (Sec. 2.1, Sec. 3.1).
  *  n_heads        H logical query heads
  *  n_groups       G native output groups; each holds one Global head
- *  d_latent       d_c, width of the latent (and of every head's value/output)
+ *  d_latent       d_c, width of the latent (the value unless value_rope)
  *  d_rope         d_r, width of the decoupled RoPE key/query part
  *  d_model        width of the projected state z
  *  n_proj_groups  n_pg: the first projection W_a is block-diagonal over n_pg
@@ -74,7 +74,16 @@ typedef enum mla_dtype { MLA_BF16 = 0, MLA_F32 = 1 } mla_dtype;
  *                 d_model, and d_model/n_pg is a multiple of 32
  *  softmax_scale  factor applied to q.k before the softmax (> 0)
  *  rope_base      RoPE base; frequency j is base^(-2j/d_r), pairs are
- *                 (x_j, x_{j+d_r/2})                                           */
+ *                 (x_j, x_{j+d_r/2})
+ *  value_rope     0: the value is the latent c, a head output has d_v = d_c
+ *                 dims and RestorePhase and the inverse output RoPE R^{-1} are
+ *                 the identity.  1 (built for (512, 64)): the value is the whole
+ *                 latent row [c ; k_r], a head output has d_v = d_c + d_r dims,
+ *                 and its RoPE part comes out relative to the query: each
+ *                 segment's canonical-frame sum is rotated by R(-(t - p_s)), i.e.
+ *                 RestorePhase R(+p_s) then R^{-1} = R(-t) (eq:offonline, Alg. 2).
+ *                 Head outputs, partials, the merge and the W_o head blocks are
+ *                 then d_v wide.                                               */
 typedef struct mla_geom {
   int32_t n_heads;
   int32_t n_groups;
@@ -84,6 +93,8 @@ typedef struct mla_geom {
   int32_t n_proj_groups;
   float softmax_scale;
   double rope_base;
+  int32_t value_rope;   /* 0: the value is the d_c latent; 1: the whole latent row
+                           (d_c + d_r, its RoPE part rotary) -- see below */
 } mla_geom;
 
 /* One document (or the request-query block) of the request (Sec. 2.3; the
@@ -129,8 +140,9 @@ mla_status mla_online_attend_query(const mla_geom* geom, const mla_segment* segs
                                    int64_t* n_slots, int64_t* n_parts, size_t* ws_bytes);
 
 /* Steps 1-2: relocation and segment-wise absorbed-MLA attention (Alg. 2,
- * SelectiveMLA with R(-Delta_i) applied to the query; RestorePhase is the
- * identity because the value is the latent and carries no rotary part).
+ * SelectiveMLA with R(-Delta_i) applied to the query; RestorePhase and R^{-1}
+ * are the identity when the value is the latent, and are applied to each
+ * segment's RoPE output dims when geom->value_rope is set).
  *  geom, segs, n_segs     host; see above
  *  prot_rows, n_prot      host int32 [P], strictly increasing storage rows (the
  *                         protected set A of eq:protected; query rows are
@@ -143,7 +155,7 @@ mla_status mla_online_attend_query(const mla_geom* geom, const mla_segment* segs
  *            relative to each segment inside the kernel)
  *  q_loc     device bf16 [P, G, hpg-1, D]: Local-head queries of protected rows
  *            (may be NULL when P == 0 or hpg == 1)
- *  part_o    device f32 [n_parts, d_c]: normalized partial outputs sum p_j c_j / sum p_j
+ *  part_o    device f32 [n_parts, d_v]: normalized partial outputs sum p_j v_j / sum p_j
  *  part_lse  device f32 [n_parts]: natural-log log-sum-exp of the scaled scores
  *  part_ptr  device i64 [n_slots + 1]: CSR offsets of each slot's partials
  *  part_seg  device i32 [n_parts, 2] or NULL: first and last segment index
@@ -162,12 +174,12 @@ mla_status mla_online_attend(const mla_geom* geom, const mla_segment* segs, int3
  * m = max l_i, w_i = exp(l_i - m), O = sum w_i o_i / sum w_i,
  * lse = m + ln sum w_i; a slot with one partial is copied.
  *  n_slots    number of slots (>= 0)
- *  d_latent   64 or 512
+ *  d_latent   head output width d_v: 64, 512, or 576 (512 + 64, rotary value)
  *  part_o, part_lse, part_ptr   device, as written by mla_online_attend
  *                               (part_ptr[0] must be 0, every slot >= 1 partial)
  *  out_dtype  MLA_BF16 or MLA_F32: element type of out_o
- *  out_o      device [n_slots, d_c]; its first N*G rows are O_glob [N, G, d_c]
- *             and the rest O_loc [P, G, hpg-1, d_c]
+ *  out_o      device [n_slots, d_v]; its first N*G rows are O_glob [N, G, d_v]
+ *             and the rest O_loc [P, G, hpg-1, d_v]
  *  out_lse    device f32 [n_slots] or NULL
  * Errors: NULL, SHAPE, UNSUPPORTED, HIP. */
 mla_status mla_segment_merge(int64_t n_slots, int32_t d_latent, const float* part_o,
@@ -177,15 +189,15 @@ mla_status mla_segment_merge(int64_t n_slots, int32_t d_latent, const float* par
 /* Step 4: z = W_{a,G} O_G + W_{a,L} O_{L,A} on protected rows, plus z_off on the
  * other rows (eq:offonline, eq:factorization; RestoreAndReplace of Alg. 2).
  * Head h of projection group pg = h / (H/n_pg) uses rows
- * [(h mod H/n_pg)*d_c, +d_c) of w_o[pg] and writes channels
+ * [(h mod H/n_pg)*d_v, +d_v) of w_o[pg] and writes channels
  * [pg*d_model/n_pg, (pg+1)*d_model/n_pg).
  *  geom        host
  *  n_rows      N
- *  o_glob      device bf16 [N, G, d_c]
- *  o_loc       device bf16 [P, G, hpg-1, d_c] (NULL allowed when P == 0 or hpg == 1)
+ *  o_glob      device bf16 [N, G, d_v]
+ *  o_loc       device bf16 [P, G, hpg-1, d_v] (NULL allowed when P == 0 or hpg == 1)
  *  glob_head   host int32 [G]: in-group index (0..hpg-1) of each group's Global head
  *  prot_rows   device int32 [P]: the same strictly increasing protected rows
- *  w_o         device bf16 [n_pg, (H/n_pg)*d_c, d_model/n_pg]
+ *  w_o         device bf16 [n_pg, (H/n_pg)*d_v, d_model/n_pg]
  *  z_off       device bf16 [N, d_model]: projected Local-head artifact; rows in
  *              the protected set are never read (NULL allowed when P == N)
  *  z           device f32 [N, d_model], written
@@ -218,7 +230,8 @@ mla_status mla_sliced_oproj_add(const mla_geom* geom, int64_t n_rows, const void
  *   z_off          [N, d_model] device, written (every element).
  *   workspace      device, 256-byte aligned, at least the size returned by
  *                  mla_offline_produce_query: plan, bf16 head outputs
- *                  [N, G, hpg-1, d_c].  Overwritten.
+ *                  [N, G, hpg-1, d_v] (and their lse with a rotary value).
+ *                  Overwritten.
  * With hpg == 1 (no Local heads) z_off is written with zeros.  Errors as for
  * mla_online_attend.
  * ------------------------------------------------------------------------- */

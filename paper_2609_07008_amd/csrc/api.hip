@@ -41,6 +41,9 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 // ---------------------------------------------------------------------------
 // validation
 // ---------------------------------------------------------------------------
+// width of one head output: the latent, plus the RoPE dims when the value is rotary
+int32_t head_dv(const mla_geom* g) { return g->d_latent + (g->value_rope ? g->d_rope : 0); }
+
 mla_status check_geom(const mla_geom* g, bool for_oproj) {
   if (g == nullptr) return fail(MLA_ERR_NULL, "geom is NULL");
   if (g->n_heads < 1 || g->n_groups < 1 || g->n_heads % g->n_groups != 0)
@@ -55,6 +58,9 @@ mla_status check_geom(const mla_geom* g, bool for_oproj) {
     return fail(MLA_ERR_SHAPE, "softmax_scale must be finite and > 0");
   if (!(g->rope_base > 1.0) || !std::isfinite(g->rope_base))
     return fail(MLA_ERR_SHAPE, "rope_base must be finite and > 1");
+  if (g->value_rope != 0 && g->value_rope != 1) return fail(MLA_ERR_SHAPE, "value_rope = %d", g->value_rope);
+  if (g->value_rope && !(g->d_latent == 512 && g->d_rope == 64))
+    return fail(MLA_ERR_UNSUPPORTED, "a rotary value is built for (d_latent, d_rope) = (512, 64)");
   if (for_oproj) {
     if (g->d_model < 1 || g->n_proj_groups < 1 || g->n_groups % g->n_proj_groups != 0 ||
         g->d_model % g->n_proj_groups != 0)
@@ -415,6 +421,7 @@ mla_status mla_online_attend(const mla_geom* geom, const mla_segment* segs, int3
   a.n_local = geom->n_groups * (hpg - 1);
   a.d_latent = geom->d_latent;
   a.d_rope = geom->d_rope;
+  a.dv = head_dv(geom);
   a.scale_log2 = geom->softmax_scale * 1.4426950408889634f;
   a.local_slot_base = p.hdr.n_rows * geom->n_groups;
   a.out_bf16 = nullptr;
@@ -431,7 +438,8 @@ mla_status mla_segment_merge(int64_t n_slots, int32_t d_latent, const float* par
                              void* stream) {
   g_detail.clear();
   if (n_slots < 0) return fail(MLA_ERR_SHAPE, "n_slots = %lld", (long long)n_slots);
-  if (d_latent != 512 && d_latent != 64) return fail(MLA_ERR_UNSUPPORTED, "d_latent %d; built: 64, 512", d_latent);
+  if (d_latent != 512 && d_latent != 64 && d_latent != 576)
+    return fail(MLA_ERR_UNSUPPORTED, "head output width %d; built: 64, 512, 576", d_latent);
   if (out_dtype != MLA_BF16 && out_dtype != MLA_F32) return fail(MLA_ERR_SHAPE, "out_dtype %d", out_dtype);
   if (n_slots == 0) return MLA_OK;
   if (part_o == nullptr || part_lse == nullptr || part_ptr == nullptr || out_o == nullptr)
@@ -473,7 +481,7 @@ mla_status mla_sliced_oproj_add(const mla_geom* geom, int64_t n_rows, const void
   a.n_prot = n_prot;
   a.n_heads = geom->n_heads;
   a.n_groups = geom->n_groups;
-  a.d_latent = geom->d_latent;
+  a.d_latent = head_dv(geom);
   a.d_model = geom->d_model;
   a.n_pg = geom->n_proj_groups;
   for (int g = 0; g < geom->n_groups; ++g) a.glob_head[g] = glob_head[g];
@@ -491,7 +499,8 @@ namespace {
 struct OfflineLayout {
   Plan plan;
   std::vector<int32_t> rows;   // identity row list: every row computes its Local heads
-  size_t off_o = 0;            // bf16 head outputs [N, G, hpg-1, d_c]
+  size_t off_o = 0;            // bf16 head outputs [N, G, hpg-1, dv]
+  size_t off_lse = 0;          // rotary value only: their lse [N, G, hpg-1] f32
   size_t total = 0;
 };
 
@@ -506,9 +515,11 @@ mla_status offline_layout(const mla_geom* geom, const mla_segment* segs, int32_t
   if ((st = build_plan(geom, segs, n_segs, L->rows.data(), (int32_t)N, 0, want_blob, &L->plan, true)) != MLA_OK)
     return st;
   const int hpg = geom->n_heads / geom->n_groups;
-  const size_t o_bytes = (size_t)N * geom->n_groups * (hpg - 1) * geom->d_latent * 2;
+  const size_t n_out = (size_t)N * geom->n_groups * (hpg - 1);
+  const size_t o_bytes = n_out * head_dv(geom) * 2;
   L->off_o = align_up((size_t)L->plan.hdr.total_bytes, 256);
-  L->total = L->off_o + align_up(o_bytes, 256);
+  L->off_lse = L->off_o + align_up(o_bytes, 256);
+  L->total = L->off_lse + (geom->value_rope ? align_up(n_out * 4, 256) : 0);
   return MLA_OK;
 }
 
@@ -569,9 +580,11 @@ mla_status mla_offline_produce(const mla_geom* geom, const mla_segment* segs, in
   a.n_local = geom->n_groups * (hpg - 1);
   a.d_latent = geom->d_latent;
   a.d_rope = geom->d_rope;
+  a.dv = head_dv(geom);
   a.scale_log2 = geom->softmax_scale * 1.4426950408889634f;
   a.local_slot_base = 0;
   a.out_bf16 = reinterpret_cast<uint16_t*>(ws + L.off_o);
+  a.part_lse = geom->value_rope ? reinterpret_cast<float*>(ws + L.off_lse) : nullptr;
   a.hdr = L.plan.hdr;
   hipError_t e = mla::launch_attend(a, s);
   if (e != hipSuccess) return hip_fail(e, "attention kernel");
@@ -587,7 +600,7 @@ mla_status mla_offline_produce(const mla_geom* geom, const mla_segment* segs, in
   op.n_prot = (int32_t)N;
   op.n_heads = geom->n_heads;
   op.n_groups = geom->n_groups;
-  op.d_latent = geom->d_latent;
+  op.d_latent = head_dv(geom);
   op.d_model = geom->d_model;
   op.n_pg = geom->n_proj_groups;
   op.z_bf16 = out_dtype == MLA_BF16 ? 1 : 0;

@@ -489,8 +489,10 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   const float l_tot = lx + ly;
   const float inv = 1.f / l_tot;
   if (a.out_bf16 != nullptr) {
-    // one chunk per slot (the offline producer): the head output itself, in bf16
-    uint16_t* ob = a.out_bf16 + slot * DC;
+    // one chunk per slot (the offline producer): the head output itself, in bf16;
+    // with a rotary value its lse too (the rotary pass normalizes with it)
+    uint16_t* ob = a.out_bf16 + slot * a.dv;
+    if (a.part_lse != nullptr && half == 0) a.part_lse[slot] = (m_run + __log2f(l_tot)) * 0.6931471805599453f;
 #pragma unroll
     for (int d = 0; d < C::OB; ++d)
 #pragma unroll
@@ -500,7 +502,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
     return;
   }
   const int64_t pidx = a.part_ptr[slot] + it.chunk;
-  float* dst = a.part_o + pidx * DC;
+  float* dst = a.part_o + pidx * a.dv;
 #pragma unroll
   for (int d = 0; d < C::OB; ++d)
 #pragma unroll
@@ -509,6 +511,302 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
       *(f32x4*)(dst + d * 32 + half * 4 + 8 * i) = v;
     }
   if (half == 0) a.part_lse[pidx] = (m_run + __log2f(l_tot)) * 0.6931471805599453f;
+}
+
+
+// ----------------------------------------------------------------------------
+// Rotary value (value = the whole latent row): the RoPE part of each head
+// output.  A second pass over the same work items and tiles: S^T = K Q^T as
+// above, weights 2^(s*scale*log2e - L) with L = the partial's log2-sum-exp
+// (already normalized), and O_r^T += K_r^T P^T for the d_r RoPE dims of the
+// tile (two 32-dim output blocks of the transposing V reads).  Each segment's
+// sum is in that segment's canonical frame; at the segment's end it is rotated
+// by R(-(t - p_s)) -- RestorePhase R(+p_s) followed by the inverse output RoPE
+// R(-t) (Alg. 2, eq:offonline) -- and added to the row's total, which is
+// written after the latent dims of the partial (or of the bf16 head output).
+// ----------------------------------------------------------------------------
+template <int DC, int DR>
+__global__ __launch_bounds__(256, 1) void attend_vrope_kernel(AttendArgs a) {
+  using C = Cfg<DC, DR>;
+  static_assert(DR == 64, "rotation pairs (j, j + 32) sit in one lane of the two RoPE output blocks");
+  __shared__ __attribute__((aligned(16))) unsigned char lds[2 * C::TILE_BYTES];
+
+  unsigned char MLA_LDS* L = (unsigned char MLA_LDS*)lds;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int half = lane >> 5, l32 = lane & 31;
+
+  const int b = blockIdx.x;
+  const int xcd = b & 7, kx = b >> 3;
+  const int item_id = (kx >> 5) * 256 + xcd * 32 + (kx & 31);
+  if (item_id >= a.n_items) return;
+
+  const unsigned char* ws = a.ws;
+  const SegInfo* segs = (const SegInfo*)(ws + a.hdr.off_segs);
+  const int32_t* rank_seg = (const int32_t*)(ws + a.hdr.off_rank);
+  const ChunkInfo* chunks = (const ChunkInfo*)(ws + a.hdr.off_chunks);
+  const WorkItem it = ((const WorkItem*)(ws + a.hdr.off_items))[item_id];
+  const int32_t* prot = (const int32_t*)(ws + a.hdr.off_prot);
+  const double* theta_rev = (const double*)(ws + a.hdr.off_theta);
+  const SegInfo own = segs[it.seg];
+  const ChunkInfo chk = chunks[own.chunk_off + it.chunk];
+
+  const int hr_local = wave * 32 + l32;
+  const bool valid = hr_local < it.count;
+  const bool active = wave * 32 < it.count;
+  const int64_t hr = it.hr_begin + (valid ? hr_local : 0);
+  int64_t row;
+  const uint16_t* qsrc;
+  int64_t slot;
+  if (it.kind == 0) {
+    row = hr / a.n_groups;
+    qsrc = (const uint16_t*)a.q_glob + hr * C::D;
+    slot = hr;
+  } else {
+    row = prot[hr / a.n_local];
+    qsrc = (const uint16_t*)a.q_loc + hr * C::D;
+    slot = a.local_slot_base + hr;
+  }
+  const int64_t t_pos = own.req_offset + (row - own.kv_start);
+  const int64_t pidx = a.out_bf16 != nullptr ? slot : a.part_ptr[slot] + it.chunk;
+  // this head-row's log2-sum-exp over the chunk (from the latent pass)
+  const float lse2 = valid ? a.part_lse[pidx] * 1.4426950408889634f : 0.f;
+
+  bf16x8 qf[C::KS];
+#pragma unroll
+  for (int ks = 0; ks < C::KS; ++ks) {
+    qf[ks] = *(const bf16x8*)(qsrc + ks * 16 + half * 8);
+    if (!valid) qf[ks] = bf16x8{};
+  }
+
+  int abase[4];
+#pragma unroll
+  for (int s4 = 0; s4 < 4; ++s4)
+    abase[s4] = (l32 >> 3) * C::KB8 + (l32 & 7) * 128 + (((2 * s4 + half) ^ rotl3(l32 & 7)) * 16);
+  const int q4 = lane >> 4, rr = (lane >> 2) & 3, cb = lane & 3;
+  const int vkey = (q4 >> 1) * 4 + rr;
+  int vb[2][2];
+#pragma unroll
+  for (int dp = 0; dp < 2; ++dp)
+#pragma unroll
+    for (int kq = 0; kq < 2; ++kq)
+      vb[dp][kq] = vkey * 128 + (((dp * 4 + (q4 & 1) * 2 + (cb >> 1)) ^ rotl3(vkey)) * 16) + (cb & 1) * 8 +
+                   kq * 4 * C::KB8;
+  const int lkey = lane >> 3;
+  const int lchunk_full = (lane & 7) ^ rotl3(lkey);
+  const int lchunk_part = (lane & 7) < (C::CH - C::CGF * 8) ? (lane & 7) : 0;
+
+  auto seg_keys = [&](const SegInfo& sg, bool is_own) -> int64_t {
+    return is_own ? (int64_t)it.max_u + 1 : sg.length;
+  };
+  auto issue = [&](unsigned char MLA_LDS* dbuf, const SegInfo& sg, int64_t n_keys, int64_t tile) {
+    const int64_t k0 = tile * C::BK;
+    const int last = (int)(n_keys - 1 - k0);
+    const bool full = last >= C::BK - 1;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int kb8 = 2 * wave + h;
+      int64_t brow = k0 + kb8 * 8;
+      int kr = lkey;
+      if (!full) {
+        const int lb = last - kb8 * 8;
+        if (lb < 0) {
+          brow = k0 + last;
+          kr = 0;
+        } else if (kr > lb) {
+          kr = lb;
+        }
+      }
+      const unsigned char* base = (const unsigned char*)a.kv + (sg.kv_start + brow) * (C::D * 2);
+      const uint32_t roff = (uint32_t)(kr * (C::D * 2));
+#pragma unroll
+      for (int cg = 0; cg < C::CG; ++cg) {
+        const int ch = cg * 8 + (cg < C::CGF ? lchunk_full : lchunk_part);
+        dma16(base, roff + ch * 16, dbuf + kb8 * C::KB8 + cg * 1024);
+      }
+    }
+  };
+
+  int c_rank = chk.first_rank;
+  SegInfo cs = segs[rank_seg[c_rank]];
+  int64_t c_tile = 0;
+  int n_rank = c_rank;
+  SegInfo ns = cs;
+  int64_t n_keys = seg_keys(cs, rank_seg[c_rank] == it.seg);
+  int64_t n_ntiles = (n_keys + C::BK - 1) / C::BK;
+  int64_t n_tile = 0;
+  int lim = 0x7fffffff, wave_lim = 0x7fffffff;
+
+  auto relocate = [&](const SegInfo& sg) {
+    const int64_t delta = t_pos - sg.req_offset;
+    const int64_t lm = delta < sg.length - 1 ? delta : sg.length - 1;
+    lim = valid ? (int)lm : 0x7fffffff;
+    wave_lim = wave_min_i(lim);
+    bf16x8 raw[C::RS];
+#pragma unroll
+    for (int rs = 0; rs < C::RS; ++rs) raw[rs] = *(const bf16x8*)(qsrc + DC + rs * 16 + half * 8);
+    const double dd = (double)delta;
+#pragma unroll
+    for (int rs = 0; rs < C::RS / 2; ++rs) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int j0 = rs * 16 + i;
+        const int prs = rs + DR / 32;
+        const double rev = dd * theta_rev[j0 + half * 8];
+        const float r = (float)(rev - rint(rev));
+        const float sn = __builtin_amdgcn_sinf(r), cn = __builtin_amdgcn_cosf(r);
+        const float x1 = (float)raw[rs][i], x2 = (float)raw[prs][i];
+        qf[C::CS + rs][i] = valid ? (__bf16)(x1 * cn - x2 * sn) : (__bf16)0.f;
+        qf[C::CS + prs][i] = valid ? (__bf16)(x1 * sn + x2 * cn) : (__bf16)0.f;
+      }
+    }
+  };
+  auto advance = [&]() -> bool {
+    if (n_tile + 1 < n_ntiles) {
+      ++n_tile;
+      return true;
+    }
+    if (n_rank >= chk.last_rank) return false;
+    ++n_rank;
+    const int sidx = rank_seg[n_rank];
+    ns = segs[sidx];
+    n_keys = seg_keys(ns, sidx == it.seg);
+    n_ntiles = (n_keys + C::BK - 1) / C::BK;
+    n_tile = 0;
+    return true;
+  };
+
+  // rope output: this segment's sum (canonical frame) and the row's total
+  f32x16 racc[2], rtot[2];
+#pragma unroll
+  for (int d = 0; d < 2; ++d)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      racc[d][e] = 0.f;
+      rtot[d][e] = 0.f;
+    }
+  // lane holds rope dims half*4 + 8i + j (reg 4i + j) of block 0 and their pair
+  // partners (+32) in block 1: rotate the pairs by R(-(t - p_s)) into the total
+  auto close_segment = [&](const SegInfo& sg) {
+    const double dd = (double)(t_pos - sg.req_offset);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int k = half * 4 + (e >> 2) * 8 + (e & 3);
+      const double rev = dd * theta_rev[k];
+      const float r = (float)(rev - rint(rev));
+      const float sn = __builtin_amdgcn_sinf(r), cn = __builtin_amdgcn_cosf(r);
+      const float x = racc[0][e], y = racc[1][e];
+      rtot[0][e] += x * cn + y * sn;
+      rtot[1][e] += y * cn - x * sn;
+      racc[0][e] = 0.f;
+      racc[1][e] = 0.f;
+    }
+  };
+
+  const float sl2 = a.scale_log2;
+  relocate(cs);
+  issue(L, cs, n_keys, 0);
+  int cur = 0;
+  for (;;) {
+    tile_barrier();
+    const bool more = advance();
+    if (more) issue(L + (C::TILE_BYTES - cur), ns, n_keys, n_tile);
+    const unsigned char MLA_LDS* buf = L + cur;
+    if (active) {
+      f32x16 s[2];
+      auto kfrag = [&](int kt, int ks) -> bf16x8 {
+        return *(const bf16x8 MLA_LDS*)(buf + abase[ks & 3] + (ks >> 2) * 1024 + kt * 4 * C::KB8);
+      };
+      bf16x8 ka[3][2];
+      ka[0][0] = kfrag(0, 0);
+      ka[0][1] = kfrag(1, 0);
+      ka[1][0] = kfrag(0, 1);
+      ka[1][1] = kfrag(1, 1);
+      // compiler-visible MFMAs here (the registers are not full): the compiler
+      // keeps the operand and result wait states itself
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        s[0][e] = 0.f;
+        s[1][e] = 0.f;
+      }
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) {
+        if (ks + 2 < C::KS) {
+          ka[(ks + 2) % 3][0] = kfrag(0, ks + 2);
+          ka[(ks + 2) % 3][1] = kfrag(1, ks + 2);
+        }
+        // the scheduling barriers keep the K reads two steps ahead of their MFMAs
+        __builtin_amdgcn_sched_barrier(0);
+        s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks % 3][0], qf[ks], s[0], 0, 0, 0);
+        s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks % 3][1], qf[ks], s[1], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      const int tk0 = (int)(c_tile * C::BK);
+      if (tk0 + C::BK - 1 > wave_lim) {
+        const int rel = lim - tk0 - ((int)(__lane_id() >> 5) << 2);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = (e >> 2) * 8 + (e & 3);
+          if (key > rel) s[0][e] = -INFINITY;
+          if (key + 32 > rel) s[1][e] = -INFINITY;
+        }
+      }
+      bf16x8 pf[C::PS];
+      const float nl = -lse2;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          pf[kt * 2 + (e >> 3)][e & 7] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][e], sl2, nl));
+      // O_r^T += K_r^T P^T: output blocks DC/32 and DC/32 + 1 of the transposing V reads
+      bf16x8 vt[C::PS][2];
+#pragma unroll
+      for (int s2 = 0; s2 < C::PS; ++s2)
+#pragma unroll
+        for (int dd = 0; dd < 2; ++dd) {
+          const int d = C::OB + dd;
+          const int off = vb[d & 1][s2 >> 1] + (d >> 1) * 1024 + (s2 & 1) * 2 * C::KB8;
+          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((MLA_LDS bf16x4*)(buf + off));
+          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((MLA_LDS bf16x4*)(buf + off + C::KB8));
+          vt[s2][dd] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+#pragma unroll
+      for (int s2 = 0; s2 < C::PS; ++s2)
+#pragma unroll
+        for (int dd = 0; dd < 2; ++dd)
+          racc[dd] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt[s2][dd], pf[s2], racc[dd], 0, 0, 0);
+    }
+    if (!more) break;
+    if (n_rank != c_rank) {
+      close_segment(cs);
+      c_rank = n_rank;
+      cs = ns;
+      relocate(cs);
+    }
+    c_tile = n_tile;
+    cur = C::TILE_BYTES - cur;
+  }
+  tile_barrier();
+  close_segment(cs);
+  if (!valid) return;
+  if (a.out_bf16 != nullptr) {
+    uint16_t* ob = a.out_bf16 + slot * a.dv + DC;
+#pragma unroll
+    for (int d = 0; d < 2; ++d)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        *(u32x2*)(ob + d * 32 + half * 4 + 8 * i) = u32x2{pack_bf16x2(rtot[d][4 * i], rtot[d][4 * i + 1]),
+                                                          pack_bf16x2(rtot[d][4 * i + 2], rtot[d][4 * i + 3])};
+    return;
+  }
+  float* dst = a.part_o + pidx * a.dv + DC;
+#pragma unroll
+  for (int d = 0; d < 2; ++d)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f32x4 v = {rtot[d][4 * i], rtot[d][4 * i + 1], rtot[d][4 * i + 2], rtot[d][4 * i + 3]};
+      *(f32x4*)(dst + d * 32 + half * 4 + 8 * i) = v;
+    }
 }
 
 // ----------------------------------------------------------------------------
@@ -590,6 +888,13 @@ hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
     attend_kernel<512, 64><<<dim3(grid), dim3(256), 0, s>>>(a);
   else if (a.d_latent == 64 && a.d_rope == 16)
     attend_kernel<64, 16><<<dim3(grid), dim3(256), 0, s>>>(a);
+  else
+    return hipErrorInvalidValue;
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.dv == a.d_latent) return e;
+  // rotary value: the RoPE dims of the head outputs, after the latent pass (its lse)
+  if (a.d_latent == 512 && a.d_rope == 64)
+    attend_vrope_kernel<512, 64><<<dim3(grid), dim3(256), 0, s>>>(a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

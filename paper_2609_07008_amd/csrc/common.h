@@ -98,10 +98,11 @@ struct AttendArgs {
   int32_t n_local;           // L_h = G*(hpg-1)
   int32_t d_latent;
   int32_t d_rope;
+  int32_t dv;                // head output width: d_latent, or d_latent + d_rope (rotary value)
   float scale_log2;          // softmax_scale * log2(e)
   int64_t local_slot_base;   // slot of Local head-row 0: n_rows * n_groups, or 0 without Global slots
   uint16_t* out_bf16;        // if set: one chunk per slot, normalized O written here as bf16
-                             // [slots, d_latent] (part_o / part_lse unused)
+                             // [slots, dv] (part_o unused; part_lse [slots] if set)
   PlanHeader hdr;            // copy of the plan header (offsets)
 };
 
@@ -134,8 +135,6 @@ struct OprojArgs {
 hipError_t launch_oproj(const OprojArgs& a, int passes, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 
-// protected token-row set (eq:protected); ws holds the storage-ordered segment
-// table, the per-row keys and the per-row flags
 // ----------------------------------------------------------------------------
 // device helpers
 // ----------------------------------------------------------------------------

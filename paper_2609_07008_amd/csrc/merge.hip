@@ -12,7 +12,8 @@ __device__ __forceinline__ float wave_max(float v) {
 }
 
 // One 64-lane wave per slot, 4 slots per 256-thread block.  Lane l owns the
-// float4 columns l, l+64, ... of the d_c-wide row.
+// float4 columns l, l+64, ... of the head-output row (d_c wide, or d_c + d_r
+// with a rotary value: the merge is linear, so both parts merge alike).
 template <int DC, bool OUT_BF16>
 __global__ __launch_bounds__(256) void merge_kernel(int64_t n_slots, const float* __restrict__ part_o,
                                                     const float* __restrict__ part_lse,
@@ -85,6 +86,11 @@ hipError_t launch_merge(int64_t n_slots, int32_t d_latent, const float* part_o, 
       merge_kernel<512, true><<<grid, block, 0, s>>>(n_slots, part_o, part_lse, part_ptr, out_o, out_lse);
     else
       merge_kernel<512, false><<<grid, block, 0, s>>>(n_slots, part_o, part_lse, part_ptr, out_o, out_lse);
+  } else if (d_latent == 576) {   // rotary value: latent and RoPE dims
+    if (bf)
+      merge_kernel<576, true><<<grid, block, 0, s>>>(n_slots, part_o, part_lse, part_ptr, out_o, out_lse);
+    else
+      merge_kernel<576, false><<<grid, block, 0, s>>>(n_slots, part_o, part_lse, part_ptr, out_o, out_lse);
   } else {
     if (bf)
       merge_kernel<64, true><<<grid, block, 0, s>>>(n_slots, part_o, part_lse, part_ptr, out_o, out_lse);

@@ -34,7 +34,7 @@ class MlaError(RuntimeError):
 class Geom(ctypes.Structure):
     _fields_ = [("n_heads", ctypes.c_int32), ("n_groups", ctypes.c_int32), ("d_latent", ctypes.c_int32),
                 ("d_rope", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_proj_groups", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float), ("rope_base", ctypes.c_double)]
+                ("softmax_scale", ctypes.c_float), ("rope_base", ctypes.c_double), ("value_rope", ctypes.c_int32)]
 
 
 class Segment(ctypes.Structure):
@@ -86,7 +86,13 @@ def _check(status: int):
 def make_geom(g) -> Geom:
     """Geometry from any object with the fields of mla_geom."""
     return Geom(int(g.n_heads), int(g.n_groups), int(g.d_latent), int(g.d_rope), int(g.d_model),
-                int(g.n_proj_groups), float(g.softmax_scale), float(g.rope_base))
+                int(g.n_proj_groups), float(g.softmax_scale), float(g.rope_base),
+                int(bool(getattr(g, "value_rope", False))))
+
+
+def head_width(g) -> int:
+    """d_v: width of one head output (d_c, or d_c + d_r with a rotary value)."""
+    return int(g.d_latent) + (int(g.d_rope) if getattr(g, "value_rope", False) else 0)
 
 
 def make_segments(segs) -> ctypes.Array:

@@ -22,7 +22,7 @@ class OnlineStep:
         self.split_keys = int(split_keys)
         self.n_rows = int(self.segs[:, 1].sum())
         self.n_slots, self.n_parts, ws = mla.attend_query(geom, self.segs, self.prot, self.split_keys)
-        d_c = int(geom.d_latent)
+        d_c = mla.head_width(geom)
         dev = torch.device(device)
         self.part_o = torch.empty((self.n_parts, d_c), dtype=torch.float32, device=dev)
         self.part_lse = torch.empty((self.n_parts,), dtype=torch.float32, device=dev)
@@ -46,7 +46,7 @@ class OnlineStep:
                           self.part_lse, self.part_ptr, self.part_seg, self.row_src, self.ws, stream)
 
     def merge(self, stream=None):
-        mla.segment_merge(self.n_slots, int(self.geom.d_latent), self.part_o, self.part_lse, self.part_ptr,
+        mla.segment_merge(self.n_slots, mla.head_width(self.geom), self.part_o, self.part_lse, self.part_ptr,
                           self.out_dtype, self.out_o, self.out_lse, stream)
 
     def oproj(self, w_o, z_off, stream=None):

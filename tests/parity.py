@@ -53,7 +53,7 @@ def compare_rows(wl, st, rows, z_off, kv=None, keys=None):
         zr = wl.z_off(rows=rows)
         zmap = {int(r): zr[i] for i, r in enumerate(rows)}
     ref = M.reference_rows(wl, rows, z_off=zmap, kv=kv, keys=keys)
-    G, hl, d_c = g.n_groups, g.heads_per_group - 1, g.d_latent
+    G, hl, d_c = g.n_groups, g.heads_per_group - 1, g.d_v
     N = wl.n_rows
     gslots = (rows[:, None] * G + np.arange(G)[None, :]).reshape(-1)
     out_o = st.out_o.float()

@@ -262,3 +262,26 @@ def test_shared_wb_rejects():
     assert call(z=None) == 1 and call(w=None) == 1 and call(y=None) == 1
     assert call(z=P(4104)) == 2
     assert call(n=0, z=None) == 0
+
+
+def test_value_rope_geometry_checks():
+    from paper_2609_07008_amd import mla
+    segs = np.array([[0, 10, 0]], dtype=np.int64)
+
+    class G:
+        n_heads, n_groups, d_latent, d_rope, d_model, n_proj_groups = 8, 2, 64, 16, 64, 2
+        softmax_scale, rope_base, value_rope = 0.1, 10000.0, True
+
+    with pytest.raises(mla.MlaError) as e:
+        mla.offline_produce_query(G, segs)
+    assert e.value.status == 3                         # rotary value: built for (512, 64) only
+    G.d_latent, G.d_rope = 512, 64
+    big = mla.offline_produce_query(G, segs)
+    G.value_rope = False
+    small = mla.offline_produce_query(G, segs)
+    assert big > small                                 # 576-wide head outputs and their lse
+    g = mla.make_geom(G)
+    g.value_rope = 2
+    ws = ctypes.c_size_t()
+    sarr, ns = mla.make_segments(segs)
+    assert mla.LIB.mla_offline_produce_query(ctypes.byref(g), sarr, ns, ctypes.byref(ws)) == 2

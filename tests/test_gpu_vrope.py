@@ -1,0 +1,80 @@
+"""GPU parity of the rotary-value variant (geom.value_rope: the value is the
+whole latent row, each segment's RoPE output restored by R(+p_s) and rotated
+back by R(-t), eq:offonline, Alg. 2) against the fp64 oracle: the 576-wide head
+outputs, lse, z_online and z of every online head, same tolerances as the
+latent-value step; the offline producer's artifact in the same variant."""
+import numpy as np
+import pytest
+
+from oracle import mla_oracle as M
+from workloads import make_custom, make_workload
+
+from parity import boundary_sample, check, check_bookkeeping, compare_rows, run
+from test_gpu_offline import produce
+
+pytestmark = pytest.mark.gpu
+
+CUSTOM = {
+    "ragged": dict(doc_lens=[1, 2, 63, 64, 65, 130, 7], req_perm=[4, 0, 6, 2, 5, 1, 3], tq=37, H=16, G=2,
+                   d_model=256, prot_frac=0.1),
+    "dense_proj": dict(doc_lens=[70, 33, 128], req_perm=[2, 0, 1], tq=20, H=16, G=2, d_model=256, n_pg=1,
+                       prot_frac=0.15),
+    "wide_groups": dict(doc_lens=[96, 40], req_perm=[1, 0], tq=9, H=32, G=4, d_model=512, prot_frac=0.2),
+    "single_segment": dict(doc_lens=[200], req_perm=None, tq=0, H=8, G=1, d_model=128, prot_frac=0.3),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CUSTOM))
+@pytest.mark.parametrize("split", [0, 100, 10 ** 9])
+@pytest.mark.parametrize("peaked", [False, True])
+def test_vrope_custom(name, split, peaked):
+    std = dict(c=1.0, kr=1.0, qc=1.0, qr=1.0, wo=0.02, zoff=0.05) if peaked else None
+    wl = make_custom(d_c=512, d_r=64, seed=700 + sorted(CUSTOM).index(name), fp32=False, std=std,
+                     value_rope=True, **CUSTOM[name])
+    assert wl.geom.d_v == 576
+    st, _ = run(wl, split)
+    check_bookkeeping(wl, st, split)
+    compare_rows(wl, st, np.arange(wl.n_rows), wl.z_off())
+
+
+@pytest.mark.parametrize("case", ["no_protected", "all_protected"])
+def test_vrope_edge_cases(case):
+    kw = dict(doc_lens=[65, 3, 64], req_perm=[1, 2, 0], tq=5, d_c=512, d_r=64, fp32=False, seed=721,
+              H=8, G=2, d_model=128, value_rope=True)
+    n = 65 + 3 + 64 + 5
+    prot = np.zeros(0, np.int32) if case == "no_protected" else np.arange(n, dtype=np.int32)
+    wl = make_custom(prot_rows=prot, **kw)
+    for split in (0, 10 ** 9):
+        st, _ = run(wl, split)
+        compare_rows(wl, st, np.arange(wl.n_rows), wl.z_off())
+
+
+@pytest.mark.parametrize("cfg,split", [(2, 0), (2, 10 ** 9), (5, 10 ** 9)])
+def test_vrope_full_workload(cfg, split):
+    wl = make_workload(cfg, value_rope=True)
+    split = min(split, wl.n_rows) if split else 0
+    st, _ = run(wl, split, with_part_seg=False)
+    g = wl.geom
+    kv = wl.kv()
+    keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    rng = np.random.default_rng(cfg)
+    rows = boundary_sample(wl) if cfg == 2 else sorted(set(
+        [int(wl.segs[s, 0]) for s in (0, 31, 63)] + [int(wl.segs[s, 0] + wl.segs[s, 1] - 1) for s in (0, 31, 63, 64)] +
+        [int(x) for x in rng.choice(wl.prot_rows, size=6, replace=False)] + [int(x) for x in rng.integers(0, wl.n_rows, 6)]))
+    compare_rows(wl, st, rows, None, kv=kv, keys=keys)
+
+
+OFFLINE = {
+    "ragged": dict(doc_lens=[1, 2, 63, 64, 65, 130, 7], req_perm=[4, 0, 6, 2, 5, 1, 3], tq=37, H=16, G=2,
+                   d_model=256),
+    "dense_proj": dict(doc_lens=[70, 33, 128], req_perm=[2, 0, 1], tq=20, H=16, G=2, d_model=256, n_pg=1),
+}
+
+
+@pytest.mark.parametrize("name", sorted(OFFLINE))
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+def test_vrope_offline_producer(name, out):
+    std = dict(c=1.0, kr=1.0, qc=1.0, qr=1.0, wo=0.02, zoff=0.05)
+    wl = make_custom(d_c=512, d_r=64, seed=740 + sorted(OFFLINE).index(name), fp32=False, std=std,
+                     value_rope=True, **OFFLINE[name])
+    check(f"z_off ({out})", produce(wl, out), M.artifact(wl))

@@ -290,9 +290,11 @@ def _std_bf16_cfg(peaked: bool, d_c: int, d_r: int):
 
 
 def make_workload(cfg: int, variant: str = "default", seed: int | None = None,
-                  n_proj_groups: int | None = None) -> Workload:
+                  n_proj_groups: int | None = None, value_rope: bool = False) -> Workload:
     """Build workload `cfg` (1..5).  variant: "default" or "peaked" (unscaled
-    queries and keys, which make the softmax far from uniform)."""
+    queries and keys, which make the softmax far from uniform).  value_rope:
+    the value is the whole latent row (cfg 2..5; W_o then has d_c + d_r rows
+    per head)."""
     if seed is None:
         seed = BASE_SEED + cfg + (1000 if variant == "peaked" else 0)
     peaked = variant == "peaked"
@@ -344,6 +346,11 @@ def make_workload(cfg: int, variant: str = "default", seed: int | None = None,
     else:
         raise ValueError(f"unknown workload {cfg}")
 
+    if value_rope:
+        if cfg == 1:
+            raise ValueError("a rotary value is built for the 512+64 latent (workloads 2..5)")
+        geom = Geometry(geom.n_heads, geom.n_groups, geom.d_latent, geom.d_rope, geom.d_model,
+                        geom.n_proj_groups, geom.softmax_scale, geom.rope_base, value_rope=True)
     segs = np.asarray(segs, dtype=np.int64)
     n = int(segs[:, 1].sum())
     qrows = np.arange(n - tq, n, dtype=np.int64)
@@ -355,7 +362,8 @@ def make_workload(cfg: int, variant: str = "default", seed: int | None = None,
              3: "32K context: 16 uneven docs at permuted offsets + 1024 query rows, 64/8 heads",
              4: "64K context: 32x2048 docs + 2048 query rows, 128 heads in 16 groups",
              5: "256K context: 64x4096 docs + 2048 query rows, 64 heads in 8 groups, 512+64 latent"}
-    return Workload(name=names[cfg] + (" (peaked)" if peaked else ""), seed=seed, geom=geom,
+    return Workload(name=names[cfg] + (" (peaked)" if peaked else "") + (", rotary value" if value_rope else ""),
+                    seed=seed, geom=geom,
                     segs=segs, glob_head=glob_head, prot_rows=prot, std=std, fp32_source=fp32,
                     random_zoff=rz, query_rows=tq, meta=dict(cfg=cfg, variant=variant))
 
