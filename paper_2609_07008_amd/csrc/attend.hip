@@ -49,6 +49,8 @@ struct Cfg {
   static_assert(kTileRows == 128, "one work item is 4 waves x 32 head-rows");
 };
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ int rotl3(int k) { return ((k << 1) | (k >> 2)) & 7; }
 
 // 16-byte direct global->LDS load: lane i writes LDS bytes [dst + 16 i, +16) of
@@ -312,16 +314,20 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
     return true;
   };
 
-  // The softmax reference max m_run is the first tile's row max.  A later tile
-  // whose row max exceeds it by more than 2^64 (weights stay below 2^64, which
-  // fp32 sums and bf16 weights hold without loss) restarts the whole item from
-  // the largest max seen so far.  A wave that sees such a tile records its index
-  // (1-based) with an LDS atomic min in restart_at; after the barrier that opens
-  // tile t every wave tests restart_at <= t, which only votes cast before that
-  // barrier can satisfy, so all waves leave the tile loop at the same tile (the
-  // tiles computed in between are discarded with the rest).  The tile loop thus
-  // never applies vector ALU work to the O accumulators, which stay in the
-  // matrix-core accumulation registers.
+  // The softmax reference m_run is the first tile's row max (log2 units), so a
+  // later tile's weights 2^(s - m_run) are not bounded by 1.  A tile in which a
+  // lane's weights sum to 2^64 or more (fp32 sums and bf16 weights hold every
+  // weight below that without loss) restarts the whole item with that row's
+  // reference raised to m_run + log2 of the larger sum of its two lanes: less
+  // than 6 above the row's max over the tile (32 keys per lane), at least 64 above
+  // m_run, so a reference that is still too low is raised again by 64 or more on
+  // the next attempt (by 128 when a weight overflowed fp32).  A wave that sees
+  // such a tile records its index (1-based) with an LDS atomic min in
+  // restart_at; after the barrier that opens tile t every wave tests restart_at
+  // <= t, which only votes cast before that barrier can satisfy, so all waves
+  // leave the tile loop at the same tile (the tiles computed in between are
+  // discarded with the rest).  The tile loop thus never applies vector ALU work
+  // to the O accumulators, which stay in the matrix-core accumulation registers.
   const float sl2 = a.scale_log2;
   float m_init = -1e30f;
   bool restarted = false;
@@ -422,28 +428,51 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
             if (key + 32 > rel) s[1][e] = -INFINITY;
           }
         }
-        float m = fmaxf(s[0][0], s[1][0]);
+        // the row max only where it sets the reference: the first tile of an item
+        auto row_max = [&]() -> float {
+          float m = fmaxf(s[0][0], s[1][0]);
 #pragma unroll
-        for (int e = 1; e < 16; ++e) m = fmaxf(m, fmaxf(s[0][e], s[1][e]));
-        float mx, my;
-        lane_halves(m, mx, my);
-        const float mt = fmaxf(mx, my) * sl2;   // row max of the tile, log2 units (sl2 > 0)
-        if (first_tile) m_run = mt;
-        m_seen = fmaxf(m_seen, mt);
-        if (__builtin_amdgcn_ballot_w64(mt > m_run + 64.f) != 0 && lane == 0) atomicMin(&restart_at, ti + 1);
+          for (int e = 1; e < 16; ++e) m = fmaxf(m, fmaxf(s[0][e], s[1][e]));
+          float mx, my;
+          lane_halves(m, mx, my);
+          return fmaxf(mx, my) * sl2;   // row max of the tile, log2 units (sl2 > 0)
+        };
+        if (first_tile) {
+          m_run = row_max();
+          m_seen = fmaxf(m_seen, m_run);
+        }
         // ---- softmax weights 2^(s*scale*log2e - m_run), rounded to bf16 in place:
         // pf[s2] is the B operand (P^T) of P.V step s2 ----
         bf16x8 pf[C::PS];
-        float rsum = 0.f;
         const float nm = -m_run;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][e], sl2, nm));
-            rsum += p;
-            pf[kt * 2 + (e >> 3)][e & 7] = (__bf16)p;
+          for (int e = 0; e < 16; ++e)
+            pf[kt * 2 + (e >> 3)][e & 7] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][e], sl2, nm));
+        // this lane's share of the row sum: the rounded weights that P.V uses, two per dot product
+        float rsum;
+        {
+          const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+          float r0 = 0.f, r1 = 0.f;
+#pragma unroll
+          for (int s2 = 0; s2 < C::PS; ++s2) {
+            // constant-index shuffles (a bit_cast of a vector element would read element 0)
+            const bf16x8 w = pf[s2];
+            r0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 0, 1), one2, r0, false);
+            r1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 2, 3), one2, r1, false);
+            r0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 4, 5), one2, r0, false);
+            r1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 6, 7), one2, r1, false);
           }
+          rsum = r0 + r1;
+        }
+        if (__builtin_amdgcn_ballot_w64(!(rsum < 0x1p64f)) != 0) {   // rare: restart vote
+          const float lr = rsum < INFINITY ? __log2f(rsum) : 128.f;
+          float ax, ay;
+          lane_halves(lr, ax, ay);
+          m_seen = fmaxf(m_seen, m_run + fmaxf(ax, ay));
+          if (lane == 0) atomicMin(&restart_at, ti + 1);
+        }
         l_run += rsum;   // this lane's keys only; the two halves are combined at the end
 
         // ---- O^T += V^T P^T over the 64 keys: 16-key steps outer, output blocks inner ----

@@ -43,8 +43,11 @@ def artifact_bf16(wl):
     return round_bf16(M.artifact(wl).astype(np.float32)).astype(np.float64)
 
 
-def compare_rows(wl, st, rows, z_off, kv=None, keys=None):
-    """Oracle vs GPU on storage rows `rows`: O and lse of every online head, z_online and z."""
+def compare_rows(wl, st, rows, z_off, kv=None, keys=None, lse_abs_tol=ABS_TOL):
+    """Oracle vs GPU on storage rows `rows`: O and lse of every online head, z_online and z.
+    `lse_abs_tol` widens the absolute bound on lse alone, for planted scores far
+    above the workload's range: the kernel rounds the relocated query to bf16,
+    so its score error (and the lse error) grows with the score itself."""
     g = wl.geom
     rows = np.asarray(sorted(set(int(r) for r in rows)), dtype=np.int64)
     if isinstance(z_off, np.ndarray):
@@ -60,7 +63,7 @@ def compare_rows(wl, st, rows, z_off, kv=None, keys=None):
     o_g = out_o[gslots].cpu().numpy().reshape(len(rows), G, d_c)
     l_g = st.out_lse[gslots].cpu().numpy().reshape(len(rows), G)
     check("O (Global heads)", o_g, ref.o_glob)
-    check("lse (Global heads)", l_g, ref.lse_glob)
+    check("lse (Global heads)", l_g, ref.lse_glob, abs_tol=lse_abs_tol)
     if ref.prot_idx:
         idx = sorted(ref.prot_idx)
         a = np.array([ref.prot_idx[i] for i in idx])
@@ -68,7 +71,7 @@ def compare_rows(wl, st, rows, z_off, kv=None, keys=None):
         o_l = out_o[lslots].cpu().numpy().reshape(len(a), G, hl, d_c)
         l_l = st.out_lse[lslots].cpu().numpy().reshape(len(a), G, hl)
         check("O (Local heads)", o_l, np.stack([ref.o_loc[i] for i in idx]))
-        check("lse (Local heads)", l_l, np.stack([ref.lse_loc[i] for i in idx]))
+        check("lse (Local heads)", l_l, np.stack([ref.lse_loc[i] for i in idx]), abs_tol=lse_abs_tol)
     z = st.z[rows].cpu().numpy().astype(np.float64)
     prot = np.isin(rows, np.asarray(wl.prot_rows))
     zoff_rows = np.stack([np.zeros(g.d_model) if p else np.asarray(zmap[int(r)], dtype=np.float64)
