@@ -8,7 +8,10 @@
 // 128 x 64 (4 x 2 MFMA 32x32x16 blocks).  K advances 64 at a time; the A and B
 // slices of a step (32 KB each) are staged into LDS with 16-byte direct
 // global->LDS loads, double-buffered, and each wave reads the fragments of the
-// next 16-wide substep while the MFMAs of the current one run.  In LDS a row of
+// next 16-wide substep while the MFMAs of the current one run.  A wave is held
+// at issue while the load path takes each direct load, so only waves 0-3 (one
+// per SIMD) issue them, 8 KB of each operand apiece: on every SIMD the partner
+// wave's MFMAs run meanwhile.  In LDS a row of
 // a slice is 8 chunks of 16 bytes, chunk c of row r stored at slot
 // c ^ ((r >> 1) & 7), so the 16-lane quarter-waves of a 16-byte fragment read
 // hit 16 distinct bank groups.  Tile order: workgroups go to the 8 XCDs
@@ -24,10 +27,11 @@ namespace {
 
 constexpr int WB_BM = 256, WB_BN = 256, WB_BK = 64;
 constexpr int WB_WAVES = 8;
+constexpr int WB_DMA_WAVES = 4;                       // waves that issue the direct loads
 constexpr int WB_ROWB = WB_BK * 2;                    // bytes of one row of a slice
 constexpr int WB_SLICE = WB_BM * WB_ROWB;             // bytes of one A (or B) slice: 32 KB
 constexpr int WB_STAGE = 2 * WB_SLICE;                // A then B
-constexpr int WB_LOADS = WB_SLICE / 1024 / WB_WAVES;  // 1 KB direct loads per wave and slice
+constexpr int WB_LOADS = WB_SLICE / 1024 / WB_DMA_WAVES;  // 1 KB direct loads per issuing wave and slice
 constexpr int WB_RPL = 1024 / WB_ROWB;                // rows per 1 KB load
 constexpr int WB_GM = 4;                              // row panels per column panel in the tile walk
 
@@ -53,7 +57,7 @@ template <bool OUT_BF16>
 __global__ __launch_bounds__(WB_WAVES * 64) void wb_gemm_kernel(WbArgs a, int m_tiles, int n_tiles) {
   constexpr int MI = 4, NI = 2, KS = WB_BK / 16;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * WB_STAGE];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   // XCD-aware, grouped tile walk
   const int total = m_tiles * n_tiles;
@@ -66,20 +70,20 @@ __global__ __launch_bounds__(WB_WAVES * 64) void wb_gemm_kernel(WbArgs a, int m_
   const int64_t m0 = (int64_t)mt * WB_BM;
   const int n0 = nt * WB_BN;
 
-  // Direct loads: load j of wave w fills LDS bytes [1024 (L w + j), +1024) of a
-  // slice (L loads per wave), i.e. rows 8 (L w + j) + lane/8 of the tile at slot
-  // lane%8, whose source is chunk (lane%8) ^ swz(row).  The load takes a
+  // Direct loads: load j of issuing wave w fills LDS bytes [1024 (L w + j), +1024)
+  // of a slice (L loads per wave), i.e. rows 8 (L w + j) + lane/8 of the tile at
+  // slot lane%8, whose source is chunk (lane%8) ^ swz(row).  The load takes a
   // wave-uniform base (the wave's first row) plus a 32-bit lane offset; a wave's
-  // rows span 32 rows, so the offsets stay below 2^32 for d_in <= 16384.  Rows
+  // rows span 64 rows, so the offsets stay below 2^32 for d_in <= 16384.  Rows
   // past the end are clamped to the last row (their results are not stored).
   const int K = a.d_in;
-  const int wr0 = WB_LOADS * WB_RPL * wave;
+  const int wr0 = WB_LOADS * WB_RPL * (wave % WB_DMA_WAVES);
   const int64_t a_base_row = std::min<int64_t>(m0 + wr0, a.n_rows - 1);
   const int64_t b_base_row = std::min<int64_t>((int64_t)n0 + wr0, (int64_t)a.d_out - 1);
   uint32_t a_lo[WB_LOADS], b_lo[WB_LOADS];
 #pragma unroll
   for (int j = 0; j < WB_LOADS; ++j) {
-    const int r = WB_RPL * (WB_LOADS * wave + j) + (lane >> 3);
+    const int r = WB_RPL * (WB_LOADS * (wave % WB_DMA_WAVES) + j) + (lane >> 3);
     const int c = (lane & 7) ^ swz(r);
     const int64_t m = std::min<int64_t>(m0 + r, a.n_rows - 1);
     const int64_t n = std::min<int64_t>((int64_t)n0 + r, (int64_t)a.d_out - 1);
@@ -90,6 +94,7 @@ __global__ __launch_bounds__(WB_WAVES * 64) void wb_gemm_kernel(WbArgs a, int m_
   const unsigned char* Bbase = (const unsigned char*)a.w_b + b_base_row * (int64_t)K * 2;
 
   auto load_slice = [&](int kt) {
+    if (wave >= WB_DMA_WAVES) return;
     unsigned char* st = lds + (kt & 1) * WB_STAGE;
     const unsigned char* ak = Abase + (int64_t)kt * WB_ROWB;
     const unsigned char* bk = Bbase + (int64_t)kt * WB_ROWB;
