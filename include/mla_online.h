@@ -197,6 +197,8 @@ mla_status mla_segment_merge(int64_t n_slots, int32_t d_latent, const float* par
  *  o_loc       device bf16 [P, G, hpg-1, d_v] (NULL allowed when P == 0 or hpg == 1)
  *  glob_head   host int32 [G]: in-group index (0..hpg-1) of each group's Global head
  *  prot_rows   device int32 [P]: the same strictly increasing protected rows
+ *              (read on the device, so not validated; an entry outside [0, N)
+ *              is skipped by the Local pass instead of being written)
  *  w_o         device bf16 [n_pg, (H/n_pg)*d_v, d_model/n_pg]
  *  z_off       device bf16 [N, d_model]: projected Local-head artifact; rows in
  *              the protected set are never read (NULL allowed when P == N)

@@ -82,8 +82,8 @@ mla_status check_segments(const mla_segment* segs, int32_t n, int64_t* n_rows) {
     if (segs[i].length < 1) return fail(MLA_ERR_SEGMENTS, "segment %d has length %lld", i, (long long)segs[i].length);
     if (segs[i].kv_start < 0 || segs[i].req_offset < 0)
       return fail(MLA_ERR_SEGMENTS, "segment %d has a negative start", i);
+    if (segs[i].length > INT32_MAX - total) return fail(MLA_ERR_UNSUPPORTED, "more than 2^31-1 rows");
     total += segs[i].length;
-    if (total > INT32_MAX) return fail(MLA_ERR_UNSUPPORTED, "more than 2^31-1 rows");
   }
   for (int pass = 0; pass < 2; ++pass) {
     std::vector<int32_t> idx(n);
@@ -198,7 +198,7 @@ mla_status build_plan(const mla_geom* g, const mla_segment* segs, int32_t n_segs
   const int64_t n_slots = (offline ? 0 : N * G) + (int64_t)n_prot * Lh;
   const int64_t n_parts = global_parts + cum_local[n_prot];
 
-  // work items: per segment, its rows' head-rows in runs of 64, times its chunks
+  // work items: per segment, its rows' head-rows in runs of kTileRows, times its chunks
   struct Cand {
     mla::WorkItem w;
     int64_t cost;
@@ -763,7 +763,8 @@ mla_status mla_shared_wb(int64_t n_rows, int32_t d_in, int32_t d_out, const void
   if (d_in > mla::kWbMaxDin) return fail(MLA_ERR_UNSUPPORTED, "d_in = %d; built: up to %d", d_in, mla::kWbMaxDin);
   if (d_out < 1) return fail(MLA_ERR_SHAPE, "d_out = %d", d_out);
   if (out_dtype != MLA_BF16 && out_dtype != MLA_F32) return fail(MLA_ERR_SHAPE, "out_dtype %d", out_dtype);
-  if ((n_rows + 255) / 256 * ((d_out + 255) / 256) > (int64_t)INT32_MAX - 8)
+  const int64_t n_tiles = (d_out - 1) / 256 + 1, m_tiles = n_rows / 256 + (n_rows % 256 != 0);
+  if (m_tiles > ((int64_t)INT32_MAX - 8) / n_tiles)
     return fail(MLA_ERR_UNSUPPORTED, "n_rows = %lld: too many tiles", (long long)n_rows);
   if (n_rows == 0) return MLA_OK;
   if (z == nullptr || w_b == nullptr || y == nullptr) return fail(MLA_ERR_NULL, "z, w_b and y are required");

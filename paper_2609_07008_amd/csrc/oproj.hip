@@ -73,6 +73,7 @@ __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_
     if (m < M) {
       if (PASS == 0) {
         orow = a.prot_rows[m];
+        if (orow < 0 || orow >= a.n_rows) orow = -1;   // outside z: the row is skipped
         flag = 1;
       } else {
         orow = (int)m;
@@ -202,6 +203,7 @@ __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_
         const int r = wm * TM + mi * 32 + half * 4 + (e >> 2) * 8 + (e & 3);
         if (m0 + r >= M) continue;
         const int64_t orow = row_out[r];
+        if (PASS == 0 && orow < 0) continue;
         float v = acc[mi][ni][e];
         if (PASS == 0 && a.z_bf16) {   // the artifact of the offline producer
           ((__bf16*)a.z)[orow * a.d_model + ch] = (__bf16)v;

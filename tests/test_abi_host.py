@@ -90,6 +90,7 @@ def _geom(wl, **over):
     ("duplicate_prot", "MLA_ERR_ROWS"),
     ("prot_out_of_range", "MLA_ERR_ROWS"),
     ("negative_split", "MLA_ERR_SHAPE"),
+    ("huge_length", "MLA_ERR_UNSUPPORTED"),
 ])
 def test_size_query_rejects(mla, case, status):
     wl = _tiny()
@@ -116,6 +117,8 @@ def test_size_query_rejects(mla, case, status):
         prot = np.concatenate([prot, [wl.n_rows]])
     elif case == "negative_split":
         split = -1
+    elif case == "huge_length":                    # the row total would overflow int64 before any tiling check
+        segs[1, 1] = np.iinfo(np.int64).max
     with pytest.raises(mla.MlaError) as ei:
         mla.attend_query(geom, segs, prot, split)
     assert mla.STATUS[ei.value.status] == status, ei.value
@@ -262,6 +265,7 @@ def test_shared_wb_rejects():
     assert call(z=None) == 1 and call(w=None) == 1 and call(y=None) == 1
     assert call(z=P(4104)) == 2
     assert call(n=0, z=None) == 0
+    assert call(n=2**62, d_out=4096) == 3 and call(n=2**63 - 1, d_out=2**31 - 1) == 3   # tile count, no overflow
 
 
 def test_value_rope_geometry_checks():
