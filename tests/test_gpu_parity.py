@@ -238,6 +238,42 @@ def test_sliced_oproj_alone(n_pg_dense):
     check("z", z.cpu().numpy(), ref, abs_tol=1e-3, rel_tol=1e-4)
 
 
+def test_sliced_oproj_skips_rows_outside_z():
+    """prot_rows is read on the device; an entry past the last row is skipped by
+    the Local pass (its o_loc row is not written anywhere), every real row is as
+    if the entry were absent."""
+    import torch
+    from paper_2609_07008_amd import device_inputs, mla
+    wl = make_custom([96, 64], req_perm=[1, 0], tq=16, H=16, G=2, d_c=512, d_r=64, d_model=256,
+                     fp32=False, seed=4, prot_frac=0.1)
+    g = wl.geom
+    rng = np.random.default_rng(8)
+    N, G, hl = wl.n_rows, g.n_groups, g.heads_per_group - 1
+    prot = np.concatenate([np.asarray(wl.prot_rows, dtype=np.int32), [N + 3]]).astype(np.int32)
+    P = prot.shape[0]
+    og = round_bf16(rng.standard_normal((N, G, g.d_latent)).astype(np.float32))
+    ol = round_bf16(rng.standard_normal((P, G, hl, g.d_latent)).astype(np.float32))
+    w_o, z_off = wl.w_o(), wl.z_off()
+    # guard band after z: rows N .. N+7 of the allocation must stay untouched
+    zbuf = torch.full((N + 8, g.d_model), 7.0, dtype=torch.float32, device="cuda")
+    mla.sliced_oproj_add(g, N, device_inputs.to_bf16(og), device_inputs.to_bf16(ol), wl.glob_head,
+                         torch.from_numpy(prot).cuda(), P, device_inputs.to_bf16(w_o), device_inputs.to_bf16(z_off),
+                         zbuf[:N])
+    torch.cuda.synchronize()
+    assert torch.all(zbuf[N:] == 7.0)
+    blocks = M.dense_blocks(w_o, g.n_heads, g.d_latent, g.d_model)
+    gid, lid = wl.global_head_ids(), wl.local_head_ids().reshape(-1)
+    prot_idx = {int(r): i for i, r in enumerate(prot[:-1])}
+    ref = np.zeros((N, g.d_model))
+    for r in range(N):
+        ref[r] = M.project(og[r], gid, blocks)
+        if r in prot_idx:
+            ref[r] += M.project(ol[prot_idx[r]].reshape(-1, g.d_latent), lid, blocks)
+        else:
+            ref[r] += z_off[r]
+    check("z", zbuf[:N].cpu().numpy(), ref, abs_tol=1e-3, rel_tol=1e-4)
+
+
 # ----------------------------------------------------------------------------
 # the five workloads at full size, in the launch configuration of the benchmark
 # ----------------------------------------------------------------------------
