@@ -166,21 +166,11 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   }
   const int64_t t_pos = own.req_offset + (row - own.kv_start);
 
-  // ---- Q fragments (B operand of S^T = K Q^T): step ks holds dims ks*16 + half*8 .. +8;
-  // for DR == 16 the RoPE step holds rope dims {half*4..+4} and {8+half*4..+4}, so that
-  // every rotation pair (j, j + d_r/2) stays inside one lane.
+  // ---- Q fragments (B operand of S^T = K Q^T), loaded once the first tile's loads
+  // are out: step ks holds dims ks*16 + half*8 .. +8; for DR == 16 the RoPE step
+  // holds rope dims {half*4..+4} and {8+half*4..+4}, so that every rotation pair
+  // (j, j + d_r/2) stays inside one lane.
   bf16x8 qf[C::KS];
-#pragma unroll
-  for (int ks = 0; ks < C::KS; ++ks) {
-    if (DR == 16 && ks == C::CS) {
-      const u32x2 lo = *(const u32x2*)(qsrc + DC + half * 4);
-      const u32x2 hi = *(const u32x2*)(qsrc + DC + 8 + half * 4);
-      qf[ks] = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
-    } else {
-      qf[ks] = *(const bf16x8*)(qsrc + ks * 16 + half * 8);
-    }
-    if (!valid) qf[ks] = bf16x8{};
-  }
 
   f32x16 o[C::OB];
   float m_run = -1e30f, l_run = 0.f;
@@ -328,6 +318,23 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   // leave the tile loop at the same tile (the tiles computed in between are
   // discarded with the rest).  The tile loop thus never applies vector ALU work
   // to the O accumulators, which stay in the matrix-core accumulation registers.
+  // the first tile's loads go out before the queries are read, so that the two
+  // latencies overlap at the start of an item
+  {
+    const SegInfo s0 = segs[rank_seg[chk.first_rank]];
+    issue(L, s0, seg_keys(s0, rank_seg[chk.first_rank] == it.seg), 0);
+  }
+#pragma unroll
+  for (int ks = 0; ks < C::KS; ++ks) {
+    if (DR == 16 && ks == C::CS) {
+      const u32x2 lo = *(const u32x2*)(qsrc + DC + half * 4);
+      const u32x2 hi = *(const u32x2*)(qsrc + DC + 8 + half * 4);
+      qf[ks] = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+    } else {
+      qf[ks] = *(const bf16x8*)(qsrc + ks * 16 + half * 8);
+    }
+    if (!valid) qf[ks] = bf16x8{};
+  }
   const float sl2 = a.scale_log2;
   float m_init = -1e30f;
   bool restarted = false;
@@ -349,7 +356,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
     n_ntiles = (n_keys + C::BK - 1) / C::BK;
     n_tile = 0;
     relocate(cs);
-    issue(L, cs, n_keys, 0);
+    if (restarted) issue(L, cs, n_keys, 0);   // the first attempt's went out before the queries
 
     bool restart = false;
     bool first_tile = !restarted;   // uniform over the workgroup
