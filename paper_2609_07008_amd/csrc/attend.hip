@@ -119,6 +119,138 @@ __device__ __forceinline__ void lane_halves(float v, float& x, float& y) {
   y = __uint_as_float(r[1]);
 }
 
+// What a work item's waves take from the plan: the tables, the item, and this
+// lane's head-row (its storage row, query, output slot and request position).
+// Blocks are dispatched round-robin over the 8 XCDs; each XCD gets 32
+// consecutive items (similar key ranges) per group of 256.
+struct ItemView {
+  const SegInfo* segs;
+  const int32_t* rank_seg;
+  const double* theta_rev;
+  WorkItem it;
+  SegInfo own;
+  ChunkInfo chk;
+  bool valid;    // this lane has a head-row
+  bool active;   // wave-uniform: the wave has head-rows
+  int64_t row, slot, t_pos;
+  const uint16_t* qsrc;
+};
+
+__device__ __forceinline__ int xcd_item_id(int b) {
+  const int xcd = b & 7, kx = b >> 3;
+  return (kx >> 5) * 256 + xcd * 32 + (kx & 31);
+}
+
+template <class C>
+__device__ __forceinline__ ItemView item_view(const AttendArgs& a, int item_id, int wave, int l32) {
+  ItemView v;
+  const unsigned char* ws = a.ws;
+  v.segs = (const SegInfo*)(ws + a.hdr.off_segs);
+  v.rank_seg = (const int32_t*)(ws + a.hdr.off_rank);
+  v.theta_rev = (const double*)(ws + a.hdr.off_theta);
+  const ChunkInfo* chunks = (const ChunkInfo*)(ws + a.hdr.off_chunks);
+  const int32_t* prot = (const int32_t*)(ws + a.hdr.off_prot);
+  v.it = ((const WorkItem*)(ws + a.hdr.off_items))[item_id];
+  v.own = v.segs[v.it.seg];
+  v.chk = chunks[v.own.chunk_off + v.it.chunk];
+  const int hr_local = wave * 32 + l32;
+  v.valid = hr_local < v.it.count;
+  v.active = wave * 32 < v.it.count;
+  const int64_t hr = v.it.hr_begin + (v.valid ? hr_local : 0);
+  if (v.it.kind == 0) {
+    v.row = hr / a.n_groups;
+    v.qsrc = (const uint16_t*)a.q_glob + hr * C::D;
+    v.slot = hr;
+  } else {
+    v.row = prot[hr / a.n_local];
+    v.qsrc = (const uint16_t*)a.q_loc + hr * C::D;
+    v.slot = a.local_slot_base + hr;
+  }
+  v.t_pos = v.own.req_offset + (v.row - v.own.kv_start);
+  return v;
+}
+
+// visible keys of segment s for the item: its own segment up to the item's last row
+__device__ __forceinline__ int64_t seg_keys(const ItemView& v, const SegInfo& s, bool is_own) {
+  return is_own ? (int64_t)v.it.max_u + 1 : s.length;
+}
+
+// Direct-to-LDS loads of tile `tile` of segment `s` (n_keys visible keys) into
+// dbuf: wave w fills key-blocks 2w, 2w+1; lane l loads key l>>3 of a block, the
+// 16-byte chunk at physical slot l&7 of each 8-chunk group.  Rows past the
+// segment's end repeat its last row.
+template <class C>
+__device__ __forceinline__ void issue_tile(const void* kv, const SegInfo& s, int64_t n_keys, int64_t tile,
+                                           unsigned char MLA_LDS* dbuf, int wave, int lkey, int lchunk_full,
+                                           int lchunk_part) {
+  const int64_t k0 = tile * C::BK;
+  const int last = (int)(n_keys - 1 - k0);
+  const bool full = last >= C::BK - 1;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int kb8 = 2 * wave + h;
+    // uniform base: first row of the 8-key block; lane offset: its key row and chunk
+    int64_t brow = k0 + kb8 * 8;
+    int kr = lkey;
+    if (!full) {
+      const int lb = last - kb8 * 8;   // last valid key of this block, relative to its first
+      if (lb < 0) {                    // whole block past the end: repeat the segment's last row
+        brow = k0 + last;
+        kr = 0;
+      } else if (kr > lb) {
+        kr = lb;
+      }
+    }
+    const unsigned char* base = (const unsigned char*)kv + (s.kv_start + brow) * (C::D * 2);
+    const uint32_t roff = (uint32_t)(kr * (C::D * 2));   // never negative
+#pragma unroll
+    for (int cg = 0; cg < C::CG; ++cg) {
+      const int ch = cg * 8 + (cg < C::CGF ? lchunk_full : lchunk_part);
+      dma16(base, roff + ch * 16, dbuf + kb8 * C::KB8 + cg * 1024);
+    }
+  }
+}
+
+// Relocation for a new segment s (Sec. 2.3 eq:rope): rotate the RoPE part of
+// this lane's query by R(t - p_s) into qf's RoPE steps; the angle is reduced in
+// double precision (in revolutions) and fed to the hardware sin/cos.  Returns
+// the lane's largest visible canonical offset in s (INT_MAX without a head-row).
+template <class C, int DC, int DR>
+__device__ __forceinline__ int relocate_query(bf16x8 (&qf)[C::KS], const ItemView& v, const SegInfo& s, int half) {
+  const int64_t delta = v.t_pos - s.req_offset;
+  const int64_t lm = delta < s.length - 1 ? delta : s.length - 1;
+  bf16x8 raw[C::RS];
+#pragma unroll
+  for (int rs = 0; rs < C::RS; ++rs) {
+    if (DR == 16) {
+      const u32x2 lo = *(const u32x2*)(v.qsrc + DC + half * 4);
+      const u32x2 hi = *(const u32x2*)(v.qsrc + DC + 8 + half * 4);
+      raw[rs] = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+    } else {
+      raw[rs] = *(const bf16x8*)(v.qsrc + DC + rs * 16 + half * 8);
+    }
+  }
+  const double dd = (double)delta;
+#pragma unroll
+  for (int rs = 0; rs < (DR == 16 ? 1 : C::RS / 2); ++rs) {
+#pragma unroll
+    for (int i = 0; i < (DR == 16 ? 4 : 8); ++i) {
+      // pair (j, j + d_r/2): first element at (rs, slot i), partner at (prs, ps)
+      const int j0 = DR == 16 ? i : rs * 16 + i;
+      const int jstep = DR == 16 ? 4 : 8;       // frequency offset of the upper lane half
+      const int prs = DR == 16 ? rs : rs + DR / 32;
+      const int ps = DR == 16 ? i + 4 : i;
+      const double rev = dd * v.theta_rev[j0 + half * jstep];
+      const float r = (float)(rev - rint(rev));
+      const float sn = __builtin_amdgcn_sinf(r), cn = __builtin_amdgcn_cosf(r);
+      const float x1 = (float)raw[rs][i], x2 = (float)raw[prs][ps];
+      qf[C::CS + rs][i] = v.valid ? (__bf16)(x1 * cn - x2 * sn) : (__bf16)0.f;
+      qf[C::CS + prs][ps] = v.valid ? (__bf16)(x1 * sn + x2 * cn) : (__bf16)0.f;
+    }
+  }
+  return v.valid ? (int)lm : 0x7fffffff;
+}
+
 template <int DC, int DR>
 __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   using C = Cfg<DC, DR>;
@@ -130,41 +262,16 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, l32 = lane & 31;
 
-  // XCD-aware item order: blocks are dispatched round-robin over the 8 XCDs;
-  // give each XCD 32 consecutive items (similar key ranges) per group of 256.
-  const int b = blockIdx.x;
-  const int xcd = b & 7, kx = b >> 3;
-  const int item_id = (kx >> 5) * 256 + xcd * 32 + (kx & 31);
+  const int item_id = xcd_item_id(blockIdx.x);
   if (item_id >= a.n_items) return;
-
-  const unsigned char* ws = a.ws;
-  const SegInfo* segs = (const SegInfo*)(ws + a.hdr.off_segs);
-  const int32_t* rank_seg = (const int32_t*)(ws + a.hdr.off_rank);
-  const ChunkInfo* chunks = (const ChunkInfo*)(ws + a.hdr.off_chunks);
-  const WorkItem it = ((const WorkItem*)(ws + a.hdr.off_items))[item_id];
-  const int32_t* prot = (const int32_t*)(ws + a.hdr.off_prot);
-  const double* theta_rev = (const double*)(ws + a.hdr.off_theta);
-  const SegInfo own = segs[it.seg];
-  const ChunkInfo chk = chunks[own.chunk_off + it.chunk];
-
-  // ---- this lane's head-row ----
-  const int hr_local = wave * 32 + l32;
-  const bool valid = hr_local < it.count;
-  const bool active = wave * 32 < it.count;   // wave-uniform: the wave has head-rows
-  const int64_t hr = it.hr_begin + (valid ? hr_local : 0);
-  int64_t row;
-  const uint16_t* qsrc;
-  int64_t slot;
-  if (it.kind == 0) {
-    row = hr / a.n_groups;
-    qsrc = (const uint16_t*)a.q_glob + hr * C::D;
-    slot = hr;
-  } else {
-    row = prot[hr / a.n_local];
-    qsrc = (const uint16_t*)a.q_loc + hr * C::D;
-    slot = a.local_slot_base + hr;
-  }
-  const int64_t t_pos = own.req_offset + (row - own.kv_start);
+  const ItemView v = item_view<C>(a, item_id, wave, l32);
+  const SegInfo* segs = v.segs;
+  const int32_t* rank_seg = v.rank_seg;
+  const WorkItem& it = v.it;
+  const ChunkInfo& chk = v.chk;
+  const bool valid = v.valid, active = v.active;
+  const int64_t slot = v.slot;
+  const uint16_t* qsrc = v.qsrc;
 
   // ---- Q fragments (B operand of S^T = K Q^T), loaded once the first tile's loads
   // are out: step ks holds dims ks*16 + half*8 .. +8; for DR == 16 the RoPE step
@@ -204,38 +311,9 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   const int lchunk_full = (lane & 7) ^ rotl3(lkey);
   const int lchunk_part = (lane & 7) < (C::CH - C::CGF * 8) ? (lane & 7) : 0;
 
-  auto seg_keys = [&](const SegInfo& s, bool is_own) -> int64_t {
-    return is_own ? (int64_t)it.max_u + 1 : s.length;
-  };
 
-  // direct-to-LDS loads of tile `tile` of segment `s`: wave w fills key-blocks 2w, 2w+1
   auto issue = [&](unsigned char MLA_LDS* dbuf, const SegInfo& s, int64_t n_keys, int64_t tile) {
-    const int64_t k0 = tile * C::BK;
-    const int last = (int)(n_keys - 1 - k0);   // rows past the segment repeat its last row
-    const bool full = last >= C::BK - 1;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int kb8 = 2 * wave + h;
-      // uniform base: first row of the 8-key block; lane offset: its key row and chunk
-      int64_t brow = k0 + kb8 * 8;
-      int kr = lkey;
-      if (!full) {
-        const int lb = last - kb8 * 8;   // last valid key of this block, relative to its first
-        if (lb < 0) {                    // whole block past the end: repeat the segment's last row
-          brow = k0 + last;
-          kr = 0;
-        } else if (kr > lb) {
-          kr = lb;
-        }
-      }
-      const unsigned char* base = (const unsigned char*)a.kv + (s.kv_start + brow) * (C::D * 2);
-      const uint32_t roff = (uint32_t)(kr * (C::D * 2));   // never negative
-#pragma unroll
-      for (int cg = 0; cg < C::CG; ++cg) {
-        const int ch = cg * 8 + (cg < C::CGF ? lchunk_full : lchunk_part);
-        dma16(base, roff + ch * 16, dbuf + kb8 * C::KB8 + cg * 1024);
-      }
-    }
+    issue_tile<C>(a.kv, s, n_keys, tile, dbuf, wave, lkey, lchunk_full, lchunk_part);
   };
 
   // ---- tile cursor over the chunk's segments (request order) ----
@@ -249,43 +327,11 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   int lim = 0x7fffffff;        // largest visible canonical offset for this lane in segment cs
   int wave_lim = 0x7fffffff;   // smallest lim over the wave's valid lanes
 
-  // relocation for a new segment: rotate the RoPE part of this lane's query by
-  // R(t - p_s); the angle is reduced in double precision (in revolutions) and
-  // fed to the hardware sin/cos
+  // relocation for a new segment: this lane's query in the segment's canonical
+  // frame, and the visibility limits of the lane and of the wave
   auto relocate = [&](const SegInfo& s) {
-    const int64_t delta = t_pos - s.req_offset;
-    const int64_t lm = delta < s.length - 1 ? delta : s.length - 1;
-    lim = valid ? (int)lm : 0x7fffffff;
+    lim = relocate_query<C, DC, DR>(qf, v, s, half);
     wave_lim = wave_min_i(lim);
-    bf16x8 raw[C::RS];
-#pragma unroll
-    for (int rs = 0; rs < C::RS; ++rs) {
-      if (DR == 16) {
-        const u32x2 lo = *(const u32x2*)(qsrc + DC + half * 4);
-        const u32x2 hi = *(const u32x2*)(qsrc + DC + 8 + half * 4);
-        raw[rs] = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
-      } else {
-        raw[rs] = *(const bf16x8*)(qsrc + DC + rs * 16 + half * 8);
-      }
-    }
-    const double dd = (double)delta;
-#pragma unroll
-    for (int rs = 0; rs < (DR == 16 ? 1 : C::RS / 2); ++rs) {
-#pragma unroll
-      for (int i = 0; i < (DR == 16 ? 4 : 8); ++i) {
-        // pair (j, j + d_r/2): first element at (rs, slot i), partner at (prs, ps)
-        const int j0 = DR == 16 ? i : rs * 16 + i;
-        const int jstep = DR == 16 ? 4 : 8;       // frequency offset of the upper lane half
-        const int prs = DR == 16 ? rs : rs + DR / 32;
-        const int ps = DR == 16 ? i + 4 : i;
-        const double rev = dd * theta_rev[j0 + half * jstep];
-        const float r = (float)(rev - rint(rev));
-        const float sn = __builtin_amdgcn_sinf(r), cn = __builtin_amdgcn_cosf(r);
-        const float x1 = (float)raw[rs][i], x2 = (float)raw[prs][ps];
-        qf[C::CS + rs][i] = valid ? (__bf16)(x1 * cn - x2 * sn) : (__bf16)0.f;
-        qf[C::CS + prs][ps] = valid ? (__bf16)(x1 * sn + x2 * cn) : (__bf16)0.f;
-      }
-    }
   };
 
   // advance the "next" cursor by one tile; returns false at the end of the chunk
@@ -298,7 +344,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
     ++n_rank;
     const int sidx = rank_seg[n_rank];
     ns = segs[sidx];
-    n_keys = seg_keys(ns, sidx == it.seg);
+    n_keys = seg_keys(v, ns, sidx == it.seg);
     n_ntiles = (n_keys + C::BK - 1) / C::BK;
     n_tile = 0;
     return true;
@@ -322,7 +368,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   // latencies overlap at the start of an item
   {
     const SegInfo s0 = segs[rank_seg[chk.first_rank]];
-    issue(L, s0, seg_keys(s0, rank_seg[chk.first_rank] == it.seg), 0);
+    issue(L, s0, seg_keys(v, s0, rank_seg[chk.first_rank] == it.seg), 0);
   }
 #pragma unroll
   for (int ks = 0; ks < C::KS; ++ks) {
@@ -352,7 +398,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
     c_tile = 0;
     n_rank = c_rank;
     ns = cs;
-    n_keys = seg_keys(cs, rank_seg[c_rank] == it.seg);
+    n_keys = seg_keys(v, cs, rank_seg[c_rank] == it.seg);
     n_ntiles = (n_keys + C::BK - 1) / C::BK;
     n_tile = 0;
     relocate(cs);
@@ -572,38 +618,17 @@ __global__ __launch_bounds__(256, 1) void attend_vrope_kernel(AttendArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, l32 = lane & 31;
 
-  const int b = blockIdx.x;
-  const int xcd = b & 7, kx = b >> 3;
-  const int item_id = (kx >> 5) * 256 + xcd * 32 + (kx & 31);
+  const int item_id = xcd_item_id(blockIdx.x);
   if (item_id >= a.n_items) return;
-
-  const unsigned char* ws = a.ws;
-  const SegInfo* segs = (const SegInfo*)(ws + a.hdr.off_segs);
-  const int32_t* rank_seg = (const int32_t*)(ws + a.hdr.off_rank);
-  const ChunkInfo* chunks = (const ChunkInfo*)(ws + a.hdr.off_chunks);
-  const WorkItem it = ((const WorkItem*)(ws + a.hdr.off_items))[item_id];
-  const int32_t* prot = (const int32_t*)(ws + a.hdr.off_prot);
-  const double* theta_rev = (const double*)(ws + a.hdr.off_theta);
-  const SegInfo own = segs[it.seg];
-  const ChunkInfo chk = chunks[own.chunk_off + it.chunk];
-
-  const int hr_local = wave * 32 + l32;
-  const bool valid = hr_local < it.count;
-  const bool active = wave * 32 < it.count;
-  const int64_t hr = it.hr_begin + (valid ? hr_local : 0);
-  int64_t row;
-  const uint16_t* qsrc;
-  int64_t slot;
-  if (it.kind == 0) {
-    row = hr / a.n_groups;
-    qsrc = (const uint16_t*)a.q_glob + hr * C::D;
-    slot = hr;
-  } else {
-    row = prot[hr / a.n_local];
-    qsrc = (const uint16_t*)a.q_loc + hr * C::D;
-    slot = a.local_slot_base + hr;
-  }
-  const int64_t t_pos = own.req_offset + (row - own.kv_start);
+  const ItemView v = item_view<C>(a, item_id, wave, l32);
+  const SegInfo* segs = v.segs;
+  const int32_t* rank_seg = v.rank_seg;
+  const WorkItem& it = v.it;
+  const ChunkInfo& chk = v.chk;
+  const bool valid = v.valid, active = v.active;
+  const int64_t slot = v.slot, t_pos = v.t_pos;
+  const uint16_t* qsrc = v.qsrc;
+  const double* theta_rev = v.theta_rev;
   const int64_t pidx = a.out_bf16 != nullptr ? slot : a.part_ptr[slot] + it.chunk;
   // this head-row's log2-sum-exp over the chunk (from the latent pass)
   const float lse2 = valid ? a.part_lse[pidx] * 1.4426950408889634f : 0.f;
@@ -632,35 +657,8 @@ __global__ __launch_bounds__(256, 1) void attend_vrope_kernel(AttendArgs a) {
   const int lchunk_full = (lane & 7) ^ rotl3(lkey);
   const int lchunk_part = (lane & 7) < (C::CH - C::CGF * 8) ? (lane & 7) : 0;
 
-  auto seg_keys = [&](const SegInfo& sg, bool is_own) -> int64_t {
-    return is_own ? (int64_t)it.max_u + 1 : sg.length;
-  };
   auto issue = [&](unsigned char MLA_LDS* dbuf, const SegInfo& sg, int64_t n_keys, int64_t tile) {
-    const int64_t k0 = tile * C::BK;
-    const int last = (int)(n_keys - 1 - k0);
-    const bool full = last >= C::BK - 1;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int kb8 = 2 * wave + h;
-      int64_t brow = k0 + kb8 * 8;
-      int kr = lkey;
-      if (!full) {
-        const int lb = last - kb8 * 8;
-        if (lb < 0) {
-          brow = k0 + last;
-          kr = 0;
-        } else if (kr > lb) {
-          kr = lb;
-        }
-      }
-      const unsigned char* base = (const unsigned char*)a.kv + (sg.kv_start + brow) * (C::D * 2);
-      const uint32_t roff = (uint32_t)(kr * (C::D * 2));
-#pragma unroll
-      for (int cg = 0; cg < C::CG; ++cg) {
-        const int ch = cg * 8 + (cg < C::CGF ? lchunk_full : lchunk_part);
-        dma16(base, roff + ch * 16, dbuf + kb8 * C::KB8 + cg * 1024);
-      }
-    }
+    issue_tile<C>(a.kv, sg, n_keys, tile, dbuf, wave, lkey, lchunk_full, lchunk_part);
   };
 
   int c_rank = chk.first_rank;
@@ -668,34 +666,14 @@ __global__ __launch_bounds__(256, 1) void attend_vrope_kernel(AttendArgs a) {
   int64_t c_tile = 0;
   int n_rank = c_rank;
   SegInfo ns = cs;
-  int64_t n_keys = seg_keys(cs, rank_seg[c_rank] == it.seg);
+  int64_t n_keys = seg_keys(v, cs, rank_seg[c_rank] == it.seg);
   int64_t n_ntiles = (n_keys + C::BK - 1) / C::BK;
   int64_t n_tile = 0;
   int lim = 0x7fffffff, wave_lim = 0x7fffffff;
 
   auto relocate = [&](const SegInfo& sg) {
-    const int64_t delta = t_pos - sg.req_offset;
-    const int64_t lm = delta < sg.length - 1 ? delta : sg.length - 1;
-    lim = valid ? (int)lm : 0x7fffffff;
+    lim = relocate_query<C, DC, DR>(qf, v, sg, half);
     wave_lim = wave_min_i(lim);
-    bf16x8 raw[C::RS];
-#pragma unroll
-    for (int rs = 0; rs < C::RS; ++rs) raw[rs] = *(const bf16x8*)(qsrc + DC + rs * 16 + half * 8);
-    const double dd = (double)delta;
-#pragma unroll
-    for (int rs = 0; rs < C::RS / 2; ++rs) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int j0 = rs * 16 + i;
-        const int prs = rs + DR / 32;
-        const double rev = dd * theta_rev[j0 + half * 8];
-        const float r = (float)(rev - rint(rev));
-        const float sn = __builtin_amdgcn_sinf(r), cn = __builtin_amdgcn_cosf(r);
-        const float x1 = (float)raw[rs][i], x2 = (float)raw[prs][i];
-        qf[C::CS + rs][i] = valid ? (__bf16)(x1 * cn - x2 * sn) : (__bf16)0.f;
-        qf[C::CS + prs][i] = valid ? (__bf16)(x1 * sn + x2 * cn) : (__bf16)0.f;
-      }
-    }
   };
   auto advance = [&]() -> bool {
     if (n_tile + 1 < n_ntiles) {
@@ -706,7 +684,7 @@ __global__ __launch_bounds__(256, 1) void attend_vrope_kernel(AttendArgs a) {
     ++n_rank;
     const int sidx = rank_seg[n_rank];
     ns = segs[sidx];
-    n_keys = seg_keys(ns, sidx == it.seg);
+    n_keys = seg_keys(v, ns, sidx == it.seg);
     n_ntiles = (n_keys + C::BK - 1) / C::BK;
     n_tile = 0;
     return true;
