@@ -331,6 +331,22 @@ def full_recompute_rows(wl, rows, kv=None, w_o=None, exact=True, q_all=None):
     return out_o, z
 
 
+def artifact_row(g, kc: np.ndarray, q_loc: np.ndarray, u: int, blocks: np.ndarray, loc) -> np.ndarray:
+    """z_off of the row at canonical position u of its segment (Alg. 1): every
+    Local head (queries q_loc [L_h, D], in the order of `loc`) attends to the
+    segment's keys u' <= u (kc: the segment's rows) with its query rotated to u,
+    and the outputs are projected by their W_o blocks."""
+    vr = bool(getattr(g, "value_rope", False))
+    dv = g.d_latent + (g.d_rope if vr else 0)
+    q = np.asarray(q_loc, dtype=F64)
+    qc = np.concatenate([q[:, :g.d_latent], rope(q[:, g.d_latent:], np.full(q.shape[0], u), g.rope_base)], axis=1)
+    scores = F64(g.softmax_scale) * (qc @ kc[: u + 1].T)
+    o, _ = softmax_stats(scores, kc[: u + 1, :dv])
+    if vr:   # canonical values carry R(u'); R^{-1} at the row's canonical position u
+        o[:, g.d_latent:] = rope(o[:, g.d_latent:], np.full(o.shape[0], -u), g.rope_base)
+    return project(o, loc, blocks)
+
+
 def artifact(wl, kv=None, q_all=None, w_o=None, exact=False) -> np.ndarray:
     """Canonical MLA-Off artifact (Alg. 1): each segment is evaluated alone with
     its first row at position 0; for each row u of a segment, every Local head
@@ -352,13 +368,7 @@ def artifact(wl, kv=None, q_all=None, w_o=None, exact=False) -> np.ndarray:
     for ks, ln, _ in np.asarray(wl.segs):
         kc = kv[ks:ks + ln]
         for u in range(ln):
-            q = np.asarray(q_all[ks + u][loc], dtype=F64)
-            qc = np.concatenate([q[:, :g.d_latent], rope(q[:, g.d_latent:], np.full(q.shape[0], u), g.rope_base)], axis=1)
-            scores = F64(g.softmax_scale) * (qc @ kc[: u + 1].T)
-            o, _ = softmax_stats(scores, kc[: u + 1, :dv])
-            if vr:   # canonical values carry R(u'); R^{-1} at the row's canonical position u
-                o[:, g.d_latent:] = rope(o[:, g.d_latent:], np.full(o.shape[0], -u), g.rope_base)
-            z_off[ks + u] = project(o, loc, blocks)
+            z_off[ks + u] = artifact_row(g, kc, q_all[ks + u][loc], u, blocks, loc)
     return z_off
 
 

@@ -77,3 +77,55 @@ def test_offline_artifact_feeds_the_online_step():
     check("z_off (bf16)", z_gpu, z_ref)
     st, _ = run(wl, 0, z_off=z_gpu)
     compare_rows(wl, st, np.arange(wl.n_rows), z_ref)
+
+
+def test_offline_full_size_sampled():
+    """The producer at the benchmark's 256K geometry and launch (64 x 4096-token
+    documents + 2048 query rows, 56 Local heads, bf16 artifact), inputs drawn on
+    the device as the benchmark draws them; sampled rows (segment starts and
+    ends, tile edges, query rows, random rows) against the oracle's canonical
+    artifact computed from the same values copied back."""
+    import torch
+    from paper_2609_07008_amd import mla
+    wl = make_workload(5)
+    g = wl.geom
+    n, hl = wl.n_rows, g.heads_per_group - 1
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(4242)
+
+    def draw(shape, std):
+        x = torch.empty(shape, dtype=torch.float32, device="cuda").normal_(0.0, 1.0, generator=gen)
+        return (x * std).to(torch.bfloat16)
+
+    kv = torch.cat([draw((n, g.d_latent), g.d_latent ** -0.5), draw((n, g.d_rope), g.d_rope ** -0.5)], 1)
+    q = torch.empty((n, g.n_groups, hl, g.d_qk), dtype=torch.bfloat16, device="cuda")
+    for c0 in range(0, n, 16384):
+        c1 = min(n, c0 + 16384)
+        q[c0:c1, :, :, :g.d_latent] = draw((c1 - c0, g.n_groups, hl, g.d_latent), g.d_latent ** -0.5)
+        q[c0:c1, :, :, g.d_latent:] = draw((c1 - c0, g.n_groups, hl, g.d_rope), g.d_rope ** -0.5)
+    rows_w = (g.n_heads // g.n_proj_groups) * g.d_latent
+    w_o = draw((g.n_proj_groups, rows_w, g.d_model // g.n_proj_groups), 0.02)
+    z = torch.full((n, g.d_model), float("nan"), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(mla.offline_produce_query(g, wl.segs), dtype=torch.uint8, device="cuda")
+    mla.offline_produce(g, wl.segs, kv, q, wl.glob_head, w_o, mla.MLA_BF16, z, ws)
+    torch.cuda.synchronize()
+
+    segs = np.asarray(wl.segs)
+    rng = np.random.default_rng(11)
+    picks = []                                   # (segment, canonical u)
+    for s in [0, 1, 31, 63]:
+        picks += [(s, u) for u in (0, 1, 63, 64, 65, 127, 2047, 4095)]
+    q_seg = int(np.argmax(segs[:, 2]))           # the query block (last in request order)
+    picks += [(q_seg, u) for u in (0, 1, 1000, int(segs[q_seg, 1]) - 1)]
+    picks += [(int(s), int(rng.integers(0, segs[s, 1]))) for s in rng.integers(0, len(segs), size=8)]
+    blocks = M.dense_blocks(w_o.float().cpu().numpy(), g.n_heads, g.d_latent, g.d_model)
+    loc = wl.local_head_ids().reshape(-1)
+    got, ref = [], []
+    for s, u in picks:
+        ks = int(segs[s, 0])
+        kc = kv[ks:ks + u + 1].float().cpu().numpy().astype(np.float64)
+        q_row = q[ks + u].float().cpu().numpy().reshape(-1, g.d_qk)
+        ref.append(M.artifact_row(g, kc, q_row, u, blocks, loc))
+        got.append(z[ks + u].float().cpu().numpy())
+    assert bool(torch.isfinite(z).all())         # every row written
+    check("z_off (bf16, 256K, sampled)", np.stack(got), np.stack(ref))
