@@ -468,8 +468,9 @@ mla_status mla_sliced_oproj_add(const mla_geom* geom, int64_t n_rows, const void
   if (n_prot > 0 && prot_rows == nullptr) return fail(MLA_ERR_NULL, "prot_rows is NULL");
   if (n_prot > 0 && hpg > 1 && o_loc == nullptr) return fail(MLA_ERR_NULL, "o_loc is NULL but Local heads exist");
   if (n_prot < n_rows && z_off == nullptr) return fail(MLA_ERR_NULL, "z_off is NULL but unprotected rows exist");
-  if (!aligned16(o_glob) || (o_loc && !aligned16(o_loc)) || !aligned16(w_o))
-    return fail(MLA_ERR_SHAPE, "o_glob, o_loc and w_o must be 16-byte aligned");
+  if (!aligned16(o_glob) || (o_loc && !aligned16(o_loc)) || !aligned16(w_o) || !aligned16(z) ||
+      (z_off && !aligned16(z_off)))
+    return fail(MLA_ERR_SHAPE, "o_glob, o_loc, w_o, z_off and z must be 16-byte aligned");
   mla::OprojArgs a{};
   a.o_glob = o_glob;
   a.o_loc = o_loc;

@@ -8,8 +8,11 @@
 //   pass G: every row, K = the Global heads of pg's groups; the epilogue adds
 //           z_off[r] on unprotected rows and the pass-L value already in z[r]
 //           on protected rows, so z_off is never read for protected rows.
-// Each head's weight rows are a d_c-row block of w_o[pg]; a K tile of 32 never
-// straddles two heads, so the B operand is gathered per tile by head.
+// Each head's weight rows are a d_c-row block of w_o[pg]; a K tile of 64 never
+// straddles two heads, so the B operand is gathered per tile by head.  The MFMAs
+// compute the transposed tile (W^T O^T), so that each lane holds one output row
+// and runs of 4 consecutive channels: the epilogue reads z_off and writes z 8 and
+// 16 bytes at a time.
 #include "common.h"
 
 #include <algorithm>
@@ -17,9 +20,9 @@
 namespace mla {
 
 // Tile shapes: BM rows x BN channels per workgroup of WM x WN waves (wave tiles
-// of multiples of 32), K in steps of 32.
-constexpr int OP_BK = 32;
-constexpr int OP_ALD = OP_BK + 8;     // padded A row (bf16): 80 B, conflict-free 16-byte row reads
+// of multiples of 32), K in steps of 64.
+constexpr int OP_BK = 64;
+constexpr int OP_ALD = OP_BK + 8;     // padded A row (bf16): 144 B, conflict-free 16-byte row reads
 
 template <int PASS, int BM, int BN, int WM, int WN>   // PASS 0 = Local over protected rows, 1 = Global
 __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
@@ -108,7 +111,7 @@ __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
       const int c = tid + NT * i;
-      const int r = c >> 2, cc = c & 3;
+      const int r = c / (OP_BK / 8), cc = c % (OP_BK / 8);
       int64_t m = m0 + r;
       if (m >= M) m = M - 1;
       ra[i] = *(const u32x4*)(A + m * lda + acol + k0 + cc * 8);
@@ -129,7 +132,7 @@ __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
       const int c = tid + NT * i;
-      *(u32x4*)(&As[buf][(c >> 2) * OP_ALD + (c & 3) * 8]) = ra[i];
+      *(u32x4*)(&As[buf][(c / (OP_BK / 8)) * OP_ALD + (c % (OP_BK / 8)) * 8]) = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
@@ -180,7 +183,7 @@ __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_
       for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bfr[ni], acc[mi][ni], 0, 0, 0);
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[ni], af[mi], acc[mi][ni], 0, 0, 0);
     }
     __syncthreads();
     if (it + 1 < nk) {
@@ -189,36 +192,41 @@ __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_
     }
   }
 
-  // epilogue: lane holds column l32 of each 32x32 block, rows half*4 + 8i + j
+  // epilogue: the accumulators hold the transposed blocks, so a lane holds output
+  // row l32 of each 32-row block and channels half*4 + 8i .. +3 of each 32-channel block
   const uint16_t* zoff = (const uint16_t*)a.z_off;
 #pragma unroll
-  for (int mi = 0; mi < MI; ++mi)
+  for (int mi = 0; mi < MI; ++mi) {
+    const int r = wm * TM + mi * 32 + l32;   // this lane's tile row
+    if (m0 + r >= M) continue;
+    const int64_t orow = row_out[r];
+    if (PASS == 0 && orow < 0) continue;
+    const int flag = row_flag[r];
 #pragma unroll
-    for (int ni = 0; ni < NI; ++ni) {
-      const int n = n0 + wn * TN + ni * 32 + l32;
-      if (n >= cw) continue;
-      const int64_t ch = (int64_t)pg * cw + n;
+    for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int r = wm * TM + mi * 32 + half * 4 + (e >> 2) * 8 + (e & 3);
-        if (m0 + r >= M) continue;
-        const int64_t orow = row_out[r];
-        if (PASS == 0 && orow < 0) continue;
-        float v = acc[mi][ni][e];
+      for (int i = 0; i < 4; ++i) {
+        const int n = n0 + wn * TN + ni * 32 + half * 4 + 8 * i;   // 4 consecutive channels
+        if (n >= cw) continue;                                     // cw is a multiple of 32
+        const int64_t off = orow * a.d_model + (int64_t)pg * cw + n;
+        f32x4 v = {acc[mi][ni][4 * i], acc[mi][ni][4 * i + 1], acc[mi][ni][4 * i + 2], acc[mi][ni][4 * i + 3]};
         if (PASS == 0 && a.z_bf16) {   // the artifact of the offline producer
-          ((__bf16*)a.z)[orow * a.d_model + ch] = (__bf16)v;
+          *(u32x2*)((uint16_t*)a.z + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
           continue;
         }
-        float* dst = a.z + orow * a.d_model + ch;
+        float* dst = a.z + off;
         if (PASS == 1) {
-          if (row_flag[r]) {
-            if (hpg > 1) v += *dst;   // the Local pass wrote this row first
-          } else
-            v += __uint_as_float((uint32_t)zoff[orow * a.d_model + ch] << 16);
+          if (flag) {
+            if (hpg > 1) v += *(const f32x4*)dst;   // the Local pass wrote this row first
+          } else {
+            const u32x2 zz = *(const u32x2*)(zoff + off);
+            v += f32x4{__uint_as_float(zz[0] << 16), __uint_as_float(zz[0] & 0xFFFF0000u),
+                       __uint_as_float(zz[1] << 16), __uint_as_float(zz[1] & 0xFFFF0000u)};
+          }
         }
-        *dst = v;
+        *(f32x4*)dst = v;
       }
-    }
+  }
 }
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(u32x4* p, int64_t n16) {

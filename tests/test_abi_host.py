@@ -168,6 +168,9 @@ def test_merge_and_oproj_reject(mla):
     assert call(g, wl.n_rows, gh, 2, None) == 1                           # z_off needed
     g2 = mla.make_geom(_geom(wl, d_model=40, n_proj_groups=2))
     assert call(g2, wl.n_rows, gh, 2, a) == 3                             # 20 channels per group
+    assert call(g, wl.n_rows, gh, 2, P((1 << 20) + 8)) == 2               # z_off misaligned (8-byte reads)
+    assert mla.LIB.mla_sliced_oproj_add(ctypes.byref(g), wl.n_rows, a, a, gh.ctypes.data_as(P), a, 2, a, a,
+                                        P((1 << 20) + 4), None) == 2      # z misaligned (16-byte writes)
 
 
 def test_offline_produce_rejects(mla):
