@@ -246,11 +246,11 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
 
 template <int PASS>
 hipError_t launch_pass(const OprojArgs& a, int64_t M, hipStream_t s) {
-  // 256 x 256 tiles, 16 waves (4 x 4 wave tiles of 64 x 64): about 78 KB of LDS,
-  // two workgroups per CU.  Same per-element K order as any other tile shape, so
-  // the results do not depend on it; measured against 128 x 128 (4 waves), 256 x 128
-  // and 128 x 256 (8 waves) at 256K, it is the fastest (4.2 vs 5.1 ms for the step's
-  // two passes, 14.5 vs 16.5 ms with every row protected).
+  // 256 x 256 tiles, 16 waves (4 x 4 wave tiles of 64 x 64): about 150 KB of LDS
+  // and up to 128 registers per wave, one workgroup per CU.  Same per-element K
+  // order as any other tile shape, so the results do not depend on it; measured
+  // against 128 x 128 (4 waves, two workgroups per CU) and 128 x 256 (8 waves) at
+  // 256K, it is as fast or faster (3.6 vs 3.65 and 3.7 ms for the step's two passes).
   constexpr int BM = 256, BN = 256, WM = 4, WN = 4;
   const int cw = a.d_model / a.n_pg;
   const int n_tiles = (cw + BN - 1) / BN;
