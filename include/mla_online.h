@@ -203,7 +203,8 @@ mla_status mla_segment_merge(int64_t n_slots, int32_t d_latent, const float* par
  *  z_off       device bf16 [N, d_model]: projected Local-head artifact; rows in
  *              the protected set are never read (NULL allowed when P == N)
  *  z           device f32 [N, d_model], written
- * Errors: NULL, SHAPE, UNSUPPORTED, ROWS, HIP. */
+ * Errors: NULL, SHAPE, UNSUPPORTED (also when N x d_model needs more than
+ * 2^31 - 8 tiles of 256 rows x 128 channels), ROWS, HIP. */
 mla_status mla_sliced_oproj_add(const mla_geom* geom, int64_t n_rows, const void* o_glob,
                                 const void* o_loc, const int32_t* glob_head,
                                 const int32_t* prot_rows, int32_t n_prot, const void* w_o,

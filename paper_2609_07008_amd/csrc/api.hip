@@ -14,6 +14,7 @@
 
 #include "common.h"
 #include "moe.h"
+#include "oproj.h"
 #include "protect.h"
 #include "wb.h"
 
@@ -471,6 +472,9 @@ mla_status mla_sliced_oproj_add(const mla_geom* geom, int64_t n_rows, const void
   if (!aligned16(o_glob) || (o_loc && !aligned16(o_loc)) || !aligned16(w_o) || !aligned16(z) ||
       (z_off && !aligned16(z_off)))
     return fail(MLA_ERR_SHAPE, "o_glob, o_loc, w_o, z_off and z must be 16-byte aligned");
+  if (mla::oproj_workgroups(n_rows, geom->d_model, geom->n_proj_groups) > INT32_MAX)
+    return fail(MLA_ERR_UNSUPPORTED, "%lld rows x d_model %d is more o-proj tiles than one launch takes",
+                (long long)n_rows, geom->d_model);
   mla::OprojArgs a{};
   a.o_glob = o_glob;
   a.o_loc = o_loc;
@@ -565,6 +569,9 @@ mla_status mla_offline_produce(const mla_geom* geom, const mla_segment* segs, in
   if (kv == nullptr || q_loc == nullptr || w_o == nullptr) return fail(MLA_ERR_NULL, "kv, q_loc and w_o are required");
   if (!aligned16(kv) || !aligned16(q_loc) || !aligned16(w_o))
     return fail(MLA_ERR_SHAPE, "kv, q_loc and w_o must be 16-byte aligned");
+  if (mla::oproj_workgroups(N, geom->d_model, geom->n_proj_groups) > INT32_MAX)
+    return fail(MLA_ERR_UNSUPPORTED, "%lld rows x d_model %d is more o-proj tiles than one launch takes",
+                (long long)N, geom->d_model);
   if ((st = upload_plan(L.plan, workspace, s)) != MLA_OK) return st;
 
   unsigned char* ws = reinterpret_cast<unsigned char*>(workspace);

@@ -113,28 +113,6 @@ hipError_t launch_merge(int64_t n_slots, int32_t d_latent, const float* part_o,
                         const float* part_lse, const int64_t* part_ptr, int32_t out_dtype,
                         void* out_o, float* out_lse, hipStream_t s);
 
-struct OprojArgs {
-  const void* o_glob;
-  const void* o_loc;
-  const int32_t* prot_rows;
-  const void* w_o;
-  const void* z_off;
-  float* z;
-  int64_t n_rows;
-  int32_t n_prot;
-  int32_t n_heads;
-  int32_t n_groups;
-  int32_t d_latent;
-  int32_t d_model;
-  int32_t n_pg;
-  int32_t z_bf16;            // 1: z is bf16 (Local pass only), 0: f32
-  int32_t glob_head[kMaxGroups];
-};
-
-// passes: bit 0 = Local heads over the protected rows, bit 1 = Global heads over all rows
-hipError_t launch_oproj(const OprojArgs& a, int passes, hipStream_t s);
-hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
-
 // ----------------------------------------------------------------------------
 // device helpers
 // ----------------------------------------------------------------------------

@@ -13,7 +13,7 @@
 // compute the transposed tile (W^T O^T), so that each lane holds one output row
 // and runs of 4 consecutive channels: the epilogue reads z_off and writes z 8 and
 // 16 bytes at a time.
-#include "common.h"
+#include "oproj.h"
 
 #include <algorithm>
 
@@ -25,7 +25,9 @@ constexpr int OP_BK = 64;
 constexpr int OP_ALD = OP_BK + 8;     // padded A row (bf16): 144 B, conflict-free 16-byte row reads
 
 template <int PASS, int BM, int BN, int WM, int WN>   // PASS 0 = Local over protected rows, 1 = Global
-__global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
+// at most 128 registers per wave, so that two workgroups of 8 waves share a CU
+__global__ __launch_bounds__(WM * WN * 64) __attribute__((amdgpu_waves_per_eu(4)))
+void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
   constexpr int NT = WM * WN * 64;
   // padded B row: 2*BLD = 64 mod 256 bytes, so the four k-rows that each half-wave
   // of a transposing read touches land on disjoint 16-bank groups (all 64 banks)
@@ -37,8 +39,10 @@ __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_
   static_assert(TM % 32 == 0 && TN % 32 == 0 && A_CH >= 1 && B_CH >= 1, "tile shape");
   static_assert(((2 * OP_BLD) % 256) == 64, "B row padding");
   constexpr int OP_BM = BM, OP_BN = BN;
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][OP_BM * OP_ALD];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][OP_BK * OP_BLD];
+  // one LDS buffer per operand: the next K step waits in registers, and two
+  // workgroups fit a CU, one's epilogue running beside the other's K loop
+  __shared__ __attribute__((aligned(16))) uint16_t As[OP_BM * OP_ALD];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[OP_BK * OP_BLD];
   __shared__ int row_flag[OP_BM];
   __shared__ int row_out[OP_BM];
 
@@ -128,16 +132,16 @@ __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_
         rb[i] = u32x4{0u, 0u, 0u, 0u};
     }
   };
-  auto store_tiles = [&](int buf) {
+  auto store_tiles = [&]() {
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
       const int c = tid + NT * i;
-      *(u32x4*)(&As[buf][(c / (OP_BK / 8)) * OP_ALD + (c % (OP_BK / 8)) * 8]) = ra[i];
+      *(u32x4*)(&As[(c / (OP_BK / 8)) * OP_ALD + (c % (OP_BK / 8)) * 8]) = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
       const int c = tid + NT * i;
-      *(u32x4*)(&Bs[buf][(c / (OP_BN / 8)) * OP_BLD + (c % (OP_BN / 8)) * 8]) = rb[i];
+      *(u32x4*)(&Bs[(c / (OP_BN / 8)) * OP_BLD + (c % (OP_BN / 8)) * 8]) = rb[i];
     }
   };
 
@@ -154,18 +158,17 @@ __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_
   const int q = lane >> 4, j16 = lane & 15;
 
   load_tiles(0);
-  store_tiles(0);
+  store_tiles();
   __syncthreads();
   const int nk = K / OP_BK;
   for (int it = 0; it < nk; ++it) {
-    const int buf = it & 1;
     if (it + 1 < nk) load_tiles((it + 1) * OP_BK);
 #pragma unroll
     for (int ks = 0; ks < OP_BK / 16; ++ks) {
       bf16x8 af[MI], bfr[NI];
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi)
-        af[mi] = *(const bf16x8*)(&As[buf][(wm * TM + mi * 32 + l32) * OP_ALD + ks * 16 + half * 8]);
+        af[mi] = *(const bf16x8*)(&As[(wm * TM + mi * 32 + l32) * OP_ALD + ks * 16 + half * 8]);
 #pragma unroll
       for (int ni = 0; ni < NI; ++ni) {
         // transposed LDS reads: lane (r*4+cb) of each 16-lane group addresses
@@ -174,9 +177,9 @@ __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_
         const int kb = ks * 16 + (q >> 1) * 8;
         const int n = wn * TN + ni * 32 + (q & 1) * 16 + cb * 4;
         const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (MLA_LDS bf16x4*)(&Bs[buf][(kb + r) * OP_BLD + n]));
+            (MLA_LDS bf16x4*)(&Bs[(kb + r) * OP_BLD + n]));
         const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (MLA_LDS bf16x4*)(&Bs[buf][(kb + 4 + r) * OP_BLD + n]));
+            (MLA_LDS bf16x4*)(&Bs[(kb + 4 + r) * OP_BLD + n]));
         bfr[ni] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       }
 #pragma unroll
@@ -187,7 +190,7 @@ __global__ __launch_bounds__(WM * WN * 64) void oproj_kernel(OprojArgs a, int m_
     }
     __syncthreads();
     if (it + 1 < nk) {
-      store_tiles(buf ^ 1);
+      store_tiles();
       __syncthreads();
     }
   }
@@ -244,14 +247,21 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
   return hipGetLastError();
 }
 
+// 256 x 128 tiles, 8 waves (4 x 2 wave tiles of 64 x 64): 58 KB of LDS and up to
+// 128 registers per wave, two workgroups per CU.  Same per-element K order as any
+// other tile shape, so the results do not depend on it.  At 256K the step's two
+// passes take 3.16 ms (128 x 256 the same; 256 x 256 with one workgroup per CU
+// 3.58, 64 x 256 with three 3.39, 128 x 128 with four 4.03 ms).
+constexpr int kOpBM = 256, kOpBN = 128, kOpWM = 4, kOpWN = 2;
+
+int64_t oproj_workgroups(int64_t M, int d_model, int n_pg) {
+  const int64_t tiles = (M + kOpBM - 1) / kOpBM * ((d_model / n_pg + kOpBN - 1) / kOpBN) * n_pg;
+  return 8 * ((tiles + 7) / 8);
+}
+
 template <int PASS>
 hipError_t launch_pass(const OprojArgs& a, int64_t M, hipStream_t s) {
-  // 256 x 256 tiles, 16 waves (4 x 4 wave tiles of 64 x 64): about 150 KB of LDS
-  // and up to 128 registers per wave, one workgroup per CU.  Same per-element K
-  // order as any other tile shape, so the results do not depend on it; measured
-  // against 128 x 128 (4 waves, two workgroups per CU) and 128 x 256 (8 waves) at
-  // 256K, it is as fast or faster (3.6 vs 3.65 and 3.7 ms for the step's two passes).
-  constexpr int BM = 256, BN = 256, WM = 4, WN = 4;
+  constexpr int BM = kOpBM, BN = kOpBN, WM = kOpWM, WN = kOpWN;
   const int cw = a.d_model / a.n_pg;
   const int n_tiles = (cw + BN - 1) / BN;
   const int m_tiles = (int)((M + BM - 1) / BM);

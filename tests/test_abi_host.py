@@ -171,6 +171,8 @@ def test_merge_and_oproj_reject(mla):
     assert call(g, wl.n_rows, gh, 2, P((1 << 20) + 8)) == 2               # z_off misaligned (8-byte reads)
     assert mla.LIB.mla_sliced_oproj_add(ctypes.byref(g), wl.n_rows, a, a, gh.ctypes.data_as(P), a, 2, a, a,
                                         P((1 << 20) + 4), None) == 2      # z misaligned (16-byte writes)
+    g3 = mla.make_geom(_geom(wl, d_model=1 << 26))
+    assert call(g3, 2**31 - 1, gh, 2, a) == 3                             # tile count beyond one launch
 
 
 def test_offline_produce_rejects(mla):
