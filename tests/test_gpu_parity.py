@@ -205,12 +205,15 @@ def test_segment_merge(d_c, out_f32):
         assert np.array_equal(got[single], po[ptr[:-1][single]])
 
 
-@pytest.mark.parametrize("n_pg_dense", [False, True])
-def test_sliced_oproj_alone(n_pg_dense):
+@pytest.mark.parametrize("n_pg,d_model", [(None, 256), (1, 256), (2, 320), (1, 96)],
+                         ids=["sliced_128", "dense_256", "sliced_160", "dense_96"])
+def test_sliced_oproj_alone(n_pg, d_model):
+    """Channels per projection group of one full 128-channel tile, two, one and a
+    ragged 32-channel tile, and one ragged tile; rows over two 256-row tiles."""
     import torch
     from paper_2609_07008_amd import device_inputs, mla
-    wl = make_custom([300, 211], req_perm=[1, 0], tq=30, H=16, G=2, d_c=512, d_r=64, d_model=256,
-                     n_pg=1 if n_pg_dense else None, fp32=False, seed=9, prot_frac=0.1)
+    wl = make_custom([300, 211], req_perm=[1, 0], tq=30, H=16, G=2, d_c=512, d_r=64, d_model=d_model,
+                     n_pg=n_pg, fp32=False, seed=9, prot_frac=0.1)
     g = wl.geom
     rng = np.random.default_rng(3)
     N, P, G, hl = wl.n_rows, wl.n_prot, g.n_groups, g.heads_per_group - 1
