@@ -25,8 +25,14 @@
  *    caller-provided workspace) and keeps no per-call state.
  *  - All device work is enqueued on `stream` (a hipStream_t passed as void*;
  *    NULL is the default stream) in call order; nothing is synchronized.  The
- *    attend call copies a small plan (segment tables and the work list) from a
- *    library-owned pinned host buffer into the workspace on the same stream.
+ *    attend, producer and protected-set calls copy a small plan (segment tables
+ *    and the work list) from a library-owned pinned host buffer into the
+ *    workspace on the same stream.
+ *  - HIP graph capture: the merge, o-proj, W_b and MoE calls enqueue kernels
+ *    only (no memset or memcpy nodes) and may be captured.  The three calls that
+ *    upload a plan return MLA_ERR_UNSUPPORTED on a capturing stream, before
+ *    enqueueing anything: their staging buffer is reused by later calls, so a
+ *    replay would not read the plan of the captured call.
  *  - Every entry point validates its arguments on the host before enqueueing
  *    anything and returns a status; it never aborts and never falls back to a
  *    different computation.  mla_last_error_detail() describes the last failure

@@ -311,8 +311,15 @@ std::mutex g_stage_mu;
 std::map<int, Staging> g_stage;
 
 mla_status upload_plan(const Plan& plan, void* ws, hipStream_t stream) {
+  // a captured copy would replay from a staging slot that later calls rewrite
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(stream, &cap);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
+  if (cap != hipStreamCaptureStatusNone)
+    return fail(MLA_ERR_UNSUPPORTED, "the stream is capturing a graph; this call uploads its plan from a "
+                "reused host staging buffer, so it runs outside capture only");
   int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
+  e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   std::lock_guard<std::mutex> lk(g_stage_mu);
   Staging& st = g_stage[dev];
