@@ -5,39 +5,17 @@ import numpy as np
 import pytest
 
 from oracle import mla_oracle as M
-from parity import check, compare_rows, run
+from parity import check, compare_rows, produce, run
 from workloads import make_custom, make_workload, round_bf16
 
 pytestmark = pytest.mark.gpu
-
-
-def produce(wl, out_dtype_name="f32"):
-    """z_off of every row from the GPU producer (float64 copy on the host)."""
-    import torch
-    from paper_2609_07008_amd import device_inputs, mla
-    g = wl.geom
-    bf16 = out_dtype_name == "bf16"
-    kv = device_inputs.to_bf16(wl.kv())
-    if g.heads_per_group > 1:
-        q = np.ascontiguousarray(wl.q_full()[:, wl.local_head_ids(), :])
-        q_loc = device_inputs.to_bf16(q)
-    else:
-        q_loc = None
-    w_o = device_inputs.to_bf16(wl.w_o())
-    ws_bytes = mla.offline_produce_query(g, wl.segs)
-    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
-    z = torch.full((wl.n_rows, g.d_model), float("nan"), dtype=torch.bfloat16 if bf16 else torch.float32,
-                   device="cuda")
-    mla.offline_produce(g, wl.segs, kv, q_loc, wl.glob_head, w_o, mla.MLA_BF16 if bf16 else mla.MLA_F32, z, ws)
-    torch.cuda.synchronize()
-    return z.float().cpu().numpy().astype(np.float64)
 
 
 @pytest.mark.parametrize("out", ["f32", "bf16"])
 @pytest.mark.parametrize("variant", ["default", "peaked"])
 def test_offline_tiny(out, variant):
     wl = make_workload(1, variant)
-    check(f"z_off ({out})", produce(wl, out), M.artifact(wl))
+    check(f"z_off ({out})", produce(wl, out), M.artifact(wl), bf16_out=out == "bf16")
 
 
 OFFLINE = {
@@ -74,7 +52,7 @@ def test_offline_artifact_feeds_the_online_step():
     wl = make_workload(1)
     z_gpu = produce(wl, "bf16")
     z_ref = round_bf16(M.artifact(wl).astype(np.float32)).astype(np.float64)
-    check("z_off (bf16)", z_gpu, z_ref)
+    check("z_off (bf16)", z_gpu, z_ref, bf16_out=True)
     st, _ = run(wl, 0, z_off=z_gpu)
     compare_rows(wl, st, np.arange(wl.n_rows), z_ref)
 
@@ -128,4 +106,4 @@ def test_offline_full_size_sampled():
         ref.append(M.artifact_row(g, kc, q_row, u, blocks, loc))
         got.append(z[ks + u].float().cpu().numpy())
     assert bool(torch.isfinite(z).all())         # every row written
-    check("z_off (bf16, 256K, sampled)", np.stack(got), np.stack(ref))
+    check("z_off (bf16, 256K, sampled)", np.stack(got), np.stack(ref), bf16_out=True)

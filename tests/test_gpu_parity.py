@@ -198,7 +198,8 @@ def test_segment_merge(d_c, out_f32):
     for s in range(len(counts)):
         ref_o[s], ref_l[s] = M.lse_merge(po[ptr[s]:ptr[s + 1]], pl[ptr[s]:ptr[s + 1]])
     got = out.float().cpu().numpy()
-    check("merged O", got, ref_o, abs_tol=2e-2 if not out_f32 else 1e-5, rel_tol=1e-2 if not out_f32 else 1e-5)
+    check("merged O", got, ref_o, abs_tol=2e-2 if not out_f32 else 1e-5, rel_tol=1e-2 if not out_f32 else 1e-5,
+          bf16_out=not out_f32)
     check("merged lse", lse.cpu().numpy(), ref_l, abs_tol=1e-4, rel_tol=1e-5)
     single = counts == 1
     if out_f32:

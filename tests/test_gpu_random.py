@@ -6,9 +6,10 @@ bit-exact.  The draw of each case depends only on its seed."""
 import numpy as np
 import pytest
 
+from oracle import mla_oracle as M
 from workloads import make_custom
 
-from parity import check_bookkeeping, compare_rows, run
+from parity import check, check_bookkeeping, compare_rows, produce, run
 
 pytestmark = pytest.mark.gpu
 
@@ -38,3 +39,14 @@ def test_random_step(seed):
     st, _ = run(wl, split)
     check_bookkeeping(wl, st, split)
     compare_rows(wl, st, np.arange(wl.n_rows), wl.z_off())
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_offline_producer(seed):
+    """The producer on the same random segment tables and head partitions (its
+    plan ignores the protected set and the split mode): z_off of every row
+    against the oracle's canonical artifact, in f32 and bf16."""
+    wl, _ = random_case(seed)
+    ref = M.artifact(wl)
+    out = "bf16" if seed % 2 else "f32"
+    check(f"z_off ({out})", produce(wl, out), ref, bf16_out=out == "bf16")

@@ -9,8 +9,7 @@ import pytest
 from oracle import mla_oracle as M
 from workloads import make_custom, make_workload
 
-from parity import boundary_sample, check, check_bookkeeping, compare_rows, run
-from test_gpu_offline import produce
+from parity import boundary_sample, check, check_bookkeeping, compare_rows, produce, run
 
 pytestmark = pytest.mark.gpu
 
@@ -77,4 +76,4 @@ def test_vrope_offline_producer(name, out):
     std = dict(c=1.0, kr=1.0, qc=1.0, qr=1.0, wo=0.02, zoff=0.05)
     wl = make_custom(d_c=512, d_r=64, seed=740 + sorted(OFFLINE).index(name), fp32=False, std=std,
                      value_rope=True, **OFFLINE[name])
-    check(f"z_off ({out})", produce(wl, out), M.artifact(wl))
+    check(f"z_off ({out})", produce(wl, out), M.artifact(wl), bf16_out=out == "bf16")
