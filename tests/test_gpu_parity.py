@@ -65,10 +65,18 @@ def test_custom_512(name, split, peaked):
     compare_rows(wl, st, np.arange(wl.n_rows), z_off)
 
 
-@pytest.mark.parametrize("case", ["no_protected", "all_protected", "all_global"])
+@pytest.mark.parametrize("case", ["no_protected", "all_protected", "all_global", "one_row", "one_row_unprotected",
+                                  "one_row_and_query"])
 def test_edge_cases(case):
     kw = dict(doc_lens=[65, 3, 64], req_perm=[1, 2, 0], tq=5, d_c=512, d_r=64, fp32=False, seed=21)
-    if case == "no_protected":
+    one = dict(doc_lens=[1], req_perm=None, d_c=512, d_r=64, fp32=False, seed=23, H=16, G=2, d_model=256)
+    if case == "one_row":                        # a one-row request: one key, every head
+        wl = make_custom(tq=0, prot_rows=np.array([0]), **one)
+    elif case == "one_row_unprotected":          # Global heads only, the artifact added
+        wl = make_custom(tq=0, prot_rows=np.zeros(0, dtype=np.int32), **one)
+    elif case == "one_row_and_query":            # a one-row document and a one-row query block
+        wl = make_custom(tq=1, **one)
+    elif case == "no_protected":
         wl = make_custom(H=16, G=2, d_model=256, prot_rows=np.zeros(0, dtype=np.int32), **kw)
     elif case == "all_protected":
         wl = make_custom(H=16, G=2, d_model=256, prot_rows=np.arange(137), **kw)
