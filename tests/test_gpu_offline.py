@@ -39,6 +39,16 @@ def test_offline_512(name, peaked):
     check("z_off", produce(wl, "f32"), M.artifact(wl))
 
 
+@pytest.mark.parametrize("tq", [0, 1])
+def test_offline_one_row_documents(tq):
+    """A request of one one-row document (and a one-row query block): every head
+    output is the single key's latent, projected by the Local heads' blocks."""
+    wl = make_custom(doc_lens=[1], req_perm=None, tq=tq, H=16, G=2, d_c=512, d_r=64, d_model=256,
+                     fp32=False, seed=33)
+    for out in ("f32", "bf16"):
+        check(f"z_off ({out})", produce(wl, out), M.artifact(wl), bf16_out=out == "bf16")
+
+
 def test_offline_without_local_heads_is_zero():
     wl = make_custom(doc_lens=[65, 3], req_perm=[1, 0], tq=5, H=4, G=4, d_c=512, d_r=64, d_model=128,
                      fp32=False, seed=31)

@@ -48,6 +48,23 @@ def test_vrope_edge_cases(case):
         compare_rows(wl, st, np.arange(wl.n_rows), wl.z_off())
 
 
+@pytest.mark.parametrize("tq,prot", [(0, [0]), (0, []), (1, None)], ids=["one_row", "one_row_unprotected",
+                                                                       "one_row_and_query"])
+def test_vrope_one_row(tq, prot):
+    """One-row requests with a rotary value: one key, so each head output is that
+    key's latent row with its RoPE part rotated back by the relative angle."""
+    kw = dict(doc_lens=[1], req_perm=None, tq=tq, d_c=512, d_r=64, fp32=False, seed=723, H=16, G=2,
+              d_model=256, value_rope=True)
+    if prot is not None:
+        kw["prot_rows"] = np.asarray(prot, dtype=np.int32)
+    wl = make_custom(**kw)
+    for split in (0, 10 ** 9):
+        st, _ = run(wl, split)
+        check_bookkeeping(wl, st, split)
+        compare_rows(wl, st, np.arange(wl.n_rows), wl.z_off())
+    check("z_off (f32)", produce(wl, "f32"), M.artifact(wl))
+
+
 @pytest.mark.parametrize("cfg,split", [(2, 0), (2, 10 ** 9), (5, 10 ** 9)])
 def test_vrope_full_workload(cfg, split):
     wl = make_workload(cfg, value_rope=True)
