@@ -43,6 +43,8 @@ SHAPES = {
     "two_k_steps": (513, 128, 300),
     "one_channel": (70, 128, 1),
     "wide": (600, 2048, 1024),
+    "one_row": (1, 64, 1),
+    "largest_d_in": (40, 16384, 70),
 }
 
 
