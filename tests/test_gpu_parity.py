@@ -185,13 +185,16 @@ def test_needle_in_the_future_is_invisible():
 # ----------------------------------------------------------------------------
 # merge and o-proj entry points on their own
 # ----------------------------------------------------------------------------
-@pytest.mark.parametrize("d_c", [64, 512])
+@pytest.mark.parametrize("d_c", [64, 512, 576])
 @pytest.mark.parametrize("out_f32", [True, False])
-def test_segment_merge(d_c, out_f32):
+@pytest.mark.parametrize("max_parts", [8, 400])
+def test_segment_merge(d_c, out_f32, max_parts):
+    """1..max_parts partials per slot (400: more than a query row of the 256K
+    workload has segments), lse spread over +-60 nats."""
     import torch
     from paper_2609_07008_amd import mla
-    rng = np.random.default_rng(5)
-    counts = rng.integers(1, 9, size=1001)
+    rng = np.random.default_rng(5 + max_parts)
+    counts = rng.integers(1, max_parts + 1, size=1001 if max_parts <= 8 else 97)
     ptr = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
     n_parts = int(ptr[-1])
     po = rng.standard_normal((n_parts, d_c)).astype(np.float32)
