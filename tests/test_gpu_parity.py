@@ -365,3 +365,26 @@ def test_full_workload_peaked(cfg):
     kv = wl.kv()
     keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
     compare_rows(wl, st, _big_sample(wl, n_seg=3), None, kv=kv, keys=keys)
+
+
+def test_optional_outputs_may_be_null():
+    """part_seg and row_src of the attend call and out_lse of the merge are
+    optional (NULL): the required outputs are then bit-identical to a run that
+    writes all of them."""
+    import torch
+    from paper_2609_07008_amd import mla
+    wl = _needle_workload(seed=37)
+    st, inp = run(wl, 0)
+    g = wl.geom
+    part_o = torch.full_like(st.part_o, float("nan"))
+    part_lse = torch.full_like(st.part_lse, float("nan"))
+    part_ptr = torch.zeros_like(st.part_ptr)
+    mla.online_attend(g, wl.segs, np.asarray(wl.prot_rows, dtype=np.int32), 0, inp["kv"], inp["q_glob"],
+                      inp["q_loc"], part_o, part_lse, part_ptr, None, None, st.ws)
+    out_o = torch.full_like(st.out_o, float("nan"))
+    mla.segment_merge(st.n_slots, g.d_latent, part_o, part_lse, part_ptr, mla.MLA_BF16, out_o, None)
+    torch.cuda.synchronize()
+    assert torch.equal(part_ptr, st.part_ptr)
+    assert torch.equal(part_o.view(torch.int32), st.part_o.view(torch.int32))
+    assert torch.equal(part_lse.view(torch.int32), st.part_lse.view(torch.int32))
+    assert torch.equal(out_o.view(torch.int16), st.out_o.view(torch.int16))
