@@ -344,6 +344,95 @@ def shared_wb_bench(torch, stream, n_rows: int, d: int = 4096, reps: int = 5):
             "TFLOP_per_s": round(flop / (ms * 1e-3) / 1e12, 1), "frac_of_bf16_peak": round(flop / (ms * 1e-3) / 2.5e15, 4)}
 
 
+def dense_oproj(wl, st, dev, torch, stream, reps: int = 5):
+    """The dense first projection (n_pg = 1: every head's 512 outputs into all
+    d_model channels) on the step's merged head outputs and protected rows, with
+    a device-drawn dense W_o [1, H*d_c, d_model] (bf16, std 0.02): the other W_a
+    layout the step supports, timed on the same rows as the grouped one."""
+    from dataclasses import replace
+    from paper_2609_07008_amd import mla
+    g = replace(wl.geom, n_proj_groups=1)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(70084)
+    w_o = (torch.randn((1, g.n_heads * g.d_latent, g.d_model), generator=gen, device="cuda") * 0.02).to(torch.bfloat16)
+    n_glob = st.n_rows * g.n_groups
+    o_glob = st.out_o[:n_glob]
+    o_loc = st.out_o[n_glob:] if st.n_slots > n_glob else None
+    z = torch.empty_like(st.z)
+    args = (g, st.n_rows, o_glob, o_loc, wl.glob_head, st.prot_d, int(st.prot.shape[0]), w_o, dev["z_off"], z)
+    mla.sliced_oproj_add(*args, stream=stream)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        mla.sliced_oproj_add(*args, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ms = float(np.median(ts))
+    head_rows = st.n_rows * g.n_groups + int(st.prot.shape[0]) * g.n_local
+    flop = head_rows * 2.0 * g.d_latent * g.d_model
+    nbytes = ((st.n_rows - int(st.prot.shape[0])) * g.d_model * 2 + st.n_rows * g.d_model * 4
+              + head_rows * g.d_latent * 2 + w_o.numel() * 2)
+    del w_o, z
+    return {"ms": round(ms, 3), "flop": flop, "TFLOP_per_s": round(flop / (ms * 1e-3) / 1e12, 1),
+            "pct_bf16_peak": round(100 * flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+            "GB_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1), "bytes": nbytes,
+            "w_o": f"dense [1, {g.n_heads * g.d_latent}, {g.d_model}] bf16"}
+
+
+class ClockSampler:
+    """Shader clock of GPU 0 sampled with rocm-smi in a background thread while
+    the timed steps run (the clock under this load decides the dense peak the
+    chip can reach: 2.5 PFLOP/s is quoted at 2.4 GHz)."""
+
+    def __init__(self):
+        import threading
+        self.samples, self.error = [], None
+        self._stop = threading.Event()
+        self._thr = threading.Thread(target=self._loop, daemon=True)
+
+    def _read(self):
+        import re
+        import subprocess
+        r = subprocess.run(["rocm-smi", "--showgpuclocks", "--json"], capture_output=True, text=True, timeout=10)
+        data = json.loads(r.stdout[r.stdout.index("{"):])
+        for card, vals in sorted(data.items()):
+            for k, v in vals.items():
+                if "sclk" in k.lower():
+                    m = re.search(r"([0-9.]+)\s*Mhz", str(v), re.I)
+                    if m:
+                        return float(m.group(1))
+        raise ValueError("no sclk field")
+
+    def _loop(self):
+        while not self._stop.is_set():
+            try:
+                self.samples.append(self._read())
+            except Exception as e:  # noqa: BLE001
+                self.error = f"{type(e).__name__}: {e}"[:200]
+                return
+            self._stop.wait(0.5)
+
+    def __enter__(self):
+        self._thr.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._thr.join(timeout=15)
+
+    def report(self):
+        out = {"source": "rocm-smi --showgpuclocks during the timed steps", "sclk_mhz": self.samples}
+        if self.samples:
+            out["median_mhz"] = float(np.median(self.samples))
+            out["peak_bf16_tflops_at_clock"] = round(PEAK_BF16_TFLOPS * out["median_mhz"] / 2400.0, 1)
+        if self.error:
+            out["error"] = self.error
+        return out
+
+
 def rotary_value_step(wl, dev, torch, stream, split: int, reps: int = 2):
     """The step with a rotary value (the value is the whole latent row; each
     segment's RoPE output dims restored and rotated back by R(-(t - p_s))) on the
@@ -447,18 +536,19 @@ def main():
 
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    for k in range(args.steps):
-        e = ev[k]
-        e[0].record(stream)
-        st.attend(dev["kv"], dev["q_glob"], dev["q_loc"])
-        e[1].record(stream)
-        st.merge()
-        e[2].record(stream)
-        st.oproj(dev["w_o"], dev["z_off"])
-        e[3].record(stream)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
+    with ClockSampler() as clock:
+        t_wall = time.perf_counter()
+        for k in range(args.steps):
+            e = ev[k]
+            e[0].record(stream)
+            st.attend(dev["kv"], dev["q_glob"], dev["q_loc"])
+            e[1].record(stream)
+            st.merge()
+            e[2].record(stream)
+            st.oproj(dev["w_o"], dev["z_off"])
+            e[3].record(stream)
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter() - t_wall
     t_att = np.median([e[0].elapsed_time(e[1]) for e in ev]) / 1e3
     t_mrg = np.median([e[1].elapsed_time(e[2]) for e in ev]) / 1e3
     t_opj = np.median([e[2].elapsed_time(e[3]) for e in ev]) / 1e3
@@ -497,6 +587,8 @@ def main():
                      "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4), "traffic": profiled_traffic(),
                      "kernel": "attend_kernel<512,64> (timed with the plan kernels of mla_online_attend)"},
     }
+    out["clock"] = clock.report()
+    out["dense_oproj"] = dense_oproj(wl, st, dev, torch, stream)
     del st
     torch.cuda.empty_cache()
     if not args.no_rotary_value:

@@ -22,6 +22,7 @@
 // 16-byte chunks of a key row are XOR-swizzled so row and column reads hit
 // distinct banks.
 #include "common.h"
+#include "restart.h"
 
 namespace mla {
 
@@ -357,7 +358,9 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   // reference raised to m_run + log2 of the larger sum of its two lanes: less
   // than 6 above the row's max over the tile (32 keys per lane), at least 64 above
   // m_run, so a reference that is still too low is raised again by 64 or more on
-  // the next attempt (by 128 when a weight overflowed fp32).  A wave that sees
+  // the next attempt (by 128 when a weight overflowed fp32).  A NaN sum never
+  // votes, and the item's last permitted attempt casts no vote at all, so the
+  // number of passes is bounded (restart.h).  A wave that sees
   // such a tile records its index (1-based) with an LDS atomic min in
   // restart_at; after the barrier that opens tile t every wave tests restart_at
   // <= t, which only votes cast before that barrier can satisfy, so all waves
@@ -384,6 +387,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   const float sl2 = a.scale_log2;
   float m_init = -1e30f;
   bool restarted = false;
+  int attempt = 0;                  // passes made over the item (workgroup-uniform)
   if (tid == 0) restart_at = ~0u;   // ordered before any access by the first tile barrier
   for (;;) {
 #pragma unroll
@@ -405,6 +409,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
     if (restarted) issue(L, cs, n_keys, 0);   // the first attempt's went out before the queries
 
     bool restart = false;
+    const bool may_vote = restart_allowed(attempt);   // uniform: the last attempt never votes
     bool first_tile = !restarted;   // uniform over the workgroup
     unsigned ti = 0;                 // tile index within the attempt (uniform)
     int cur = 0;
@@ -519,11 +524,10 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
           }
           rsum = r0 + r1;
         }
-        if (__builtin_amdgcn_ballot_w64(!(rsum < 0x1p64f)) != 0) {   // rare: restart vote
-          const float lr = rsum < INFINITY ? __log2f(rsum) : 128.f;
+        if (__builtin_amdgcn_ballot_w64(may_vote && restart_vote(rsum)) != 0) {   // rare: restart vote
           float ax, ay;
-          lane_halves(lr, ax, ay);
-          m_seen = fmaxf(m_seen, m_run + fmaxf(ax, ay));
+          lane_halves(restart_raise(rsum), ax, ay);
+          m_seen = raised_reference(m_seen, m_run, ax, ay);
           if (lane == 0) atomicMin(&restart_at, ti + 1);
         }
         l_run += rsum;   // this lane's keys only; the two halves are combined at the end
@@ -562,6 +566,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
     if (tid == 0) restart_at = ~0u;
     m_init = m_seen;
     restarted = true;
+    ++attempt;
   }
 
   // ---- epilogue: combine the two lane halves' row sums, store normalized partial and lse ----

@@ -131,3 +131,18 @@ def produce(wl, out_dtype_name="f32"):
     mla.offline_produce(g, wl.segs, kv, q_loc, wl.glob_head, w_o, mla.MLA_BF16 if bf16 else mla.MLA_F32, z, ws)
     torch.cuda.synchronize()
     return z.float().cpu().numpy().astype(np.float64)
+
+
+def segment_edge_sample(wl, n_prot=32, n_rand=8, seed=1):
+    """Rows for the full-size comparisons: the first and last row of every
+    segment (where relocation angles and chunk boundaries change), `n_prot`
+    protected rows (every head online) and `n_rand` uniform rows; seeded."""
+    rng = np.random.default_rng(seed)
+    rows = set()
+    for ks, ln, _ in wl.segs:
+        rows.update([int(ks), int(ks + ln - 1)])
+    prot = np.asarray(wl.prot_rows)
+    if prot.size:
+        rows.update(int(x) for x in rng.choice(prot, size=min(n_prot, prot.size), replace=False))
+    rows.update(int(x) for x in rng.integers(0, wl.n_rows, size=n_rand))
+    return sorted(rows)

@@ -10,7 +10,8 @@ import pytest
 from oracle import mla_oracle as M
 from workloads import make_custom, make_workload, round_bf16
 
-from parity import artifact_bf16, boundary_sample, check, check_bookkeeping, compare_rows, run
+from parity import (artifact_bf16, boundary_sample, check, check_bookkeeping, compare_rows, run,
+                    segment_edge_sample)
 
 pytestmark = pytest.mark.gpu
 
@@ -327,31 +328,22 @@ def test_sliced_oproj_skips_rows_outside_z():
 # ----------------------------------------------------------------------------
 # the five workloads at full size, in the launch configuration of the benchmark
 # ----------------------------------------------------------------------------
-def _big_sample(wl, n_seg=6, seed=1):
-    rng = np.random.default_rng(seed)
-    order = np.argsort(wl.segs[:, 2])
-    pick = list(order[:2]) + list(order[-2:]) + list(rng.choice(order, size=n_seg, replace=False))
-    rows = set()
-    for s in pick:
-        ks, ln, _ = wl.segs[s]
-        rows.update([int(ks), int(ks + ln - 1)])
-    prot = np.asarray(wl.prot_rows)
-    rows.update(int(x) for x in rng.choice(prot, size=6, replace=False))
-    rows.update(int(x) for x in rng.integers(0, wl.n_rows, size=4))
-    return sorted(rows)
-
-
-@pytest.mark.parametrize("cfg,split", [(2, 0), (2, 10 ** 9), (3, 8192), (3, 10 ** 9), (4, 10 ** 9),
-                                       (5, 10 ** 9)])
-def test_full_workload(cfg, split):
-    wl = make_workload(cfg)
+@pytest.mark.parametrize("cfg,split,n_pg", [(2, 0, None), (2, 10 ** 9, None), (2, 0, 1), (2, 10 ** 9, 1),
+                                            (3, 8192, None), (3, 10 ** 9, None), (4, 10 ** 9, None),
+                                            (5, 10 ** 9, None)])
+def test_full_workload(cfg, split, n_pg):
+    """Each workload at full size; n_pg = 1 is the dense first projection
+    (K = 64 heads x 512 into all 4096 channels) on the 8 x 4096 + 256 workload.
+    Per-segment partials are compared on the boundary sample; the other launches
+    on the first and last row of every segment plus 32 protected rows."""
+    wl = make_workload(cfg, n_proj_groups=n_pg)
     split = min(split, wl.n_rows) if split else 0
     st, _ = run(wl, split, with_part_seg=(cfg <= 3))
     check_bookkeeping(wl, st, split, full_part_seg=(cfg <= 3))
     g = wl.geom
     kv = wl.kv()
     keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
-    rows = boundary_sample(wl) if cfg <= 3 and split == 0 else _big_sample(wl, n_seg=3 if cfg >= 4 else 6)
+    rows = boundary_sample(wl) if cfg <= 3 and split == 0 else segment_edge_sample(wl)
     compare_rows(wl, st, rows, None, kv=kv, keys=keys)
 
 
@@ -364,7 +356,7 @@ def test_full_workload_peaked(cfg):
     g = wl.geom
     kv = wl.kv()
     keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
-    compare_rows(wl, st, _big_sample(wl, n_seg=3), None, kv=kv, keys=keys)
+    compare_rows(wl, st, segment_edge_sample(wl, n_prot=16, seed=2), None, kv=kv, keys=keys)
 
 
 def test_optional_outputs_may_be_null():

@@ -9,7 +9,7 @@ import pytest
 from oracle import mla_oracle as M
 from workloads import make_custom, make_workload
 
-from parity import boundary_sample, check, check_bookkeeping, compare_rows, produce, run
+from parity import boundary_sample, check, check_bookkeeping, compare_rows, produce, run, segment_edge_sample
 
 pytestmark = pytest.mark.gpu
 
@@ -73,10 +73,7 @@ def test_vrope_full_workload(cfg, split):
     g = wl.geom
     kv = wl.kv()
     keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
-    rng = np.random.default_rng(cfg)
-    rows = boundary_sample(wl) if cfg == 2 else sorted(set(
-        [int(wl.segs[s, 0]) for s in (0, 31, 63)] + [int(wl.segs[s, 0] + wl.segs[s, 1] - 1) for s in (0, 31, 63, 64)] +
-        [int(x) for x in rng.choice(wl.prot_rows, size=6, replace=False)] + [int(x) for x in rng.integers(0, wl.n_rows, 6)]))
+    rows = boundary_sample(wl) if cfg == 2 else segment_edge_sample(wl, n_prot=32, seed=cfg)
     compare_rows(wl, st, rows, None, kv=kv, keys=keys)
 
 
