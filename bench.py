@@ -2,9 +2,12 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 5] [--split-keys S]
 
-A step is one pass of the whole path over the 256K-context workload:
-mla_online_attend (plan + relocation + segment-wise attention), mla_segment_merge
-and mla_sliced_oproj_add, with every input already resident in HBM.  Prints one
+A step is one pass of the whole path over the 256K-context workload, with every
+input already resident in HBM and the plan for the segment table built once
+beforehand (mla_online_plan): mla_online_attend_planned (device half of the plan
+from the device-resident protected set, relocation, segment-wise attention with
+the merge done by online rescaling, bf16 head outputs) and
+mla_sliced_oproj_add_planned (sliced o-proj with the artifact add, f32 z).  Prints one
 JSON line.  `value` is achieved TFLOP/s of attention + o-proj algorithmic work
 over the whole step; `roofline` reports the attention kernel alone against the
 dense bf16 MFMA peak; `cpu_baseline` times the fp64 oracle on a bounded row
@@ -317,14 +320,15 @@ def moe_fanout_bench(torch, stream, n_rows: int, n_experts: int = 256, tau: floa
             "mean_fanout": round(float(k.float().mean().item()), 4)}
 
 
-def shared_wb_bench(torch, stream, n_rows: int, d: int = 4096, reps: int = 5):
-    """mla_shared_wb: y = W_b z over every row of the workload (z [N, 4096] bf16
-    drawn on the device, W_b [4096, 4096] bf16 with std 0.02, y fp32): median time
-    and the MFMA rate against the dense bf16 peak."""
+def shared_wb_bench(torch, stream, z, reps: int = 5):
+    """mla_shared_wb: y = W_b z over every row of the workload, z the step's own
+    bf16 output (mla_sliced_oproj_add_planned with a bf16 z), W_b [4096, 4096]
+    bf16 with std 0.02 drawn on the device, y fp32: median time and the MFMA
+    rate against the dense bf16 peak."""
     from paper_2609_07008_amd import mla
+    n_rows, d = int(z.shape[0]), int(z.shape[1])
     g = torch.Generator(device="cuda")
     g.manual_seed(70082)
-    z = (torch.randn((n_rows, d), generator=g, device="cuda") * 0.05).to(torch.bfloat16)
     w = (torch.randn((d, d), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
     y = torch.empty((n_rows, d), dtype=torch.float32, device="cuda")
     mla.shared_wb(z, w, y, stream=stream)
@@ -339,12 +343,12 @@ def shared_wb_bench(torch, stream, n_rows: int, d: int = 4096, reps: int = 5):
         ts.append(e0.elapsed_time(e1))
     ms = float(np.median(ts))
     flop = 2.0 * n_rows * d * d
-    del z, w, y
-    return {"rows": n_rows, "d_in": d, "d_out": d, "ms": round(ms, 3), "flop": flop,
+    del w, y
+    return {"rows": n_rows, "d_in": d, "d_out": d, "ms": round(ms, 3), "flop": flop, "z": "the step's bf16 z",
             "TFLOP_per_s": round(flop / (ms * 1e-3) / 1e12, 1), "frac_of_bf16_peak": round(flop / (ms * 1e-3) / 2.5e15, 4)}
 
 
-def dense_oproj(wl, st, dev, torch, stream, reps: int = 5):
+def dense_oproj(wl, out_o, dev, torch, stream, reps: int = 5):
     """The dense first projection (n_pg = 1: every head's 512 outputs into all
     d_model channels) on the step's merged head outputs and protected rows, with
     a device-drawn dense W_o [1, H*d_c, d_model] (bf16, std 0.02): the other W_a
@@ -355,11 +359,13 @@ def dense_oproj(wl, st, dev, torch, stream, reps: int = 5):
     gen = torch.Generator(device="cuda")
     gen.manual_seed(70084)
     w_o = (torch.randn((1, g.n_heads * g.d_latent, g.d_model), generator=gen, device="cuda") * 0.02).to(torch.bfloat16)
-    n_glob = st.n_rows * g.n_groups
-    o_glob = st.out_o[:n_glob]
-    o_loc = st.out_o[n_glob:] if st.n_slots > n_glob else None
-    z = torch.empty_like(st.z)
-    args = (g, st.n_rows, o_glob, o_loc, wl.glob_head, st.prot_d, int(st.prot.shape[0]), w_o, dev["z_off"], z)
+    n_rows, n_prot = wl.n_rows, wl.n_prot
+    n_glob = n_rows * g.n_groups
+    o_glob = out_o[:n_glob]
+    o_loc = out_o[n_glob:n_glob + n_prot * g.n_local] if n_prot * g.n_local else None
+    z = torch.empty((n_rows, g.d_model), dtype=torch.float32, device="cuda")
+    prot_d = torch.from_numpy(np.ascontiguousarray(wl.prot_rows, dtype=np.int32)).cuda()
+    args = (g, n_rows, o_glob, o_loc, wl.glob_head, prot_d, n_prot, w_o, dev["z_off"], z)
     mla.sliced_oproj_add(*args, stream=stream)
     torch.cuda.synchronize()
     ts = []
@@ -371,15 +377,44 @@ def dense_oproj(wl, st, dev, torch, stream, reps: int = 5):
         torch.cuda.synchronize()
         ts.append(e0.elapsed_time(e1))
     ms = float(np.median(ts))
-    head_rows = st.n_rows * g.n_groups + int(st.prot.shape[0]) * g.n_local
+    head_rows = n_rows * g.n_groups + n_prot * g.n_local
     flop = head_rows * 2.0 * g.d_latent * g.d_model
-    nbytes = ((st.n_rows - int(st.prot.shape[0])) * g.d_model * 2 + st.n_rows * g.d_model * 4
-              + head_rows * g.d_latent * 2 + w_o.numel() * 2)
+    nbytes = ((n_rows - n_prot) * g.d_model * 2 + n_rows * g.d_model * 4 + head_rows * g.d_latent * 2
+              + w_o.numel() * 2)
     del w_o, z
     return {"ms": round(ms, 3), "flop": flop, "TFLOP_per_s": round(flop / (ms * 1e-3) / 1e12, 1),
             "pct_bf16_peak": round(100 * flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
             "GB_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1), "bytes": nbytes,
             "w_o": f"dense [1, {g.n_heads * g.d_latent}, {g.d_model}] bf16"}
+
+
+def host_plan_step(wl, dev, torch, stream, split: int, reps: int = 3):
+    """The same step through the host-plan entry points (mla_online_attend, which
+    builds and uploads its plan from the host on every call, writes f32 partials,
+    then mla_segment_merge and mla_sliced_oproj_add), for comparison with the
+    plan-once path that the headline times."""
+    from paper_2609_07008_amd import step
+    st = step.OnlineStep(wl.geom, wl.segs, wl.prot_rows, wl.glob_head, split, with_part_seg=False)
+    st.run(dev["kv"], dev["q_glob"], dev["q_loc"], dev["w_o"], dev["z_off"])
+    torch.cuda.synchronize()
+    t = []
+    for _ in range(reps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record(stream)
+        st.attend(dev["kv"], dev["q_glob"], dev["q_loc"])
+        e[1].record(stream)
+        st.merge()
+        e[2].record(stream)
+        st.oproj(dev["w_o"], dev["z_off"])
+        e[3].record(stream)
+        torch.cuda.synchronize()
+        t.append([e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3]), e[0].elapsed_time(e[3])])
+    t = np.median(np.asarray(t), axis=0)
+    out = {"ms": {"attend": round(float(t[0]), 3), "merge": round(float(t[1]), 3), "oproj": round(float(t[2]), 3),
+                  "step": round(float(t[3]), 3)}, "partials": st.n_parts}
+    del st
+    torch.cuda.empty_cache()
+    return out
 
 
 class ClockSampler:
@@ -448,21 +483,20 @@ def rotary_value_step(wl, dev, torch, stream, split: int, reps: int = 2):
     hp = g.n_heads // g.n_proj_groups
     w_o = (torch.randn((g.n_proj_groups, hp * dv, g.d_model // g.n_proj_groups), generator=gen, device="cuda")
            * 0.02).to(torch.bfloat16)
-    st = step.OnlineStep(g, wl.segs, wl.prot_rows, wl.glob_head, split, with_part_seg=False)
-    st.run(dev["kv"], dev["q_glob"], dev["q_loc"], w_o, dev["z_off"])
+    st = step.PlannedStep(g, wl.segs, wl.glob_head, split, wl.n_rows, bookkeeping=False)
+    prot_d, n_d = dev["prot_d"], dev["n_prot_d"]
+    st.run(prot_d, n_d, dev["kv"], dev["q_glob"], dev["q_loc"], w_o, dev["z_off"])
     torch.cuda.synchronize()
     t = []
     for _ in range(reps):
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
         e[0].record(stream)
-        st.attend(dev["kv"], dev["q_glob"], dev["q_loc"])
+        st.attend(prot_d, n_d, dev["kv"], dev["q_glob"], dev["q_loc"])
         e[1].record(stream)
-        st.merge()
+        st.oproj(prot_d, n_d, w_o, dev["z_off"])
         e[2].record(stream)
-        st.oproj(w_o, dev["z_off"])
-        e[3].record(stream)
         torch.cuda.synchronize()
-        t.append([e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3]), e[0].elapsed_time(e[3])])
+        t.append([e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[0].elapsed_time(e[2])])
     t = np.median(np.asarray(t), axis=0)
     pos = wl.row_position()
     prot = np.asarray(wl.prot_rows, dtype=np.int64)
@@ -470,9 +504,8 @@ def rotary_value_step(wl, dev, torch, stream, split: int, reps: int = 2):
     flop_attn = vis * (2.0 * (g.d_latent + g.d_rope) + 2.0 * dv)
     head_rows = wl.n_rows * g.n_groups + len(prot) * g.n_local
     flop_oproj = head_rows * 2.0 * dv * g.d_model / g.n_proj_groups
-    ms = float(t[3])
-    out = {"ms": {"attend": round(float(t[0]), 3), "merge": round(float(t[1]), 3), "oproj": round(float(t[2]), 3),
-                  "step": round(ms, 3)},
+    ms = float(t[2])
+    out = {"ms": {"attend": round(float(t[0]), 3), "oproj": round(float(t[1]), 3), "step": round(ms, 3)},
            "flop": flop_attn + flop_oproj,
            "TFLOP_per_s": round((flop_attn + flop_oproj) / (ms * 1e-3) / 1e12, 1),
            "pct_bf16_peak": round(100 * (flop_attn + flop_oproj) / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
@@ -497,6 +530,8 @@ def main():
     ap.add_argument("--no-offline-producer", action="store_true",
                     help="skip the MLA-Off producer measurement on the same geometry")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--prot-cap", type=int, default=-1,
+                    help="capacity of the plan for the protected set; -1 = every row")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -526,37 +561,40 @@ def main():
     dev = device_inputs.upload(wl)
     torch.cuda.synchronize()
     t_upload = time.perf_counter() - t0
-    st = step.OnlineStep(g, wl.segs, wl.prot_rows, wl.glob_head, split, with_part_seg=False)
+    # plan once for the segment table, capacity = every row; the protected set
+    # lives on the device and each step only enqueues kernels
+    dev["prot_d"] = torch.from_numpy(np.ascontiguousarray(wl.prot_rows, dtype=np.int32)).cuda()
+    dev["n_prot_d"] = torch.tensor([wl.n_prot], dtype=torch.int32, device="cuda")
+    prot_cap = wl.n_rows if args.prot_cap < 0 else args.prot_cap
+    st = step.PlannedStep(g, wl.segs, wl.glob_head, split, prot_cap, bookkeeping=False)
     flop_attn, flop_oproj, head_rows = algorithmic_work(wl)
+    prot_d, n_d = dev["prot_d"], dev["n_prot_d"]
 
     stream = torch.cuda.current_stream()
     for _ in range(args.warmup):
-        st.run(dev["kv"], dev["q_glob"], dev["q_loc"], dev["w_o"], dev["z_off"])
+        st.run(prot_d, n_d, dev["kv"], dev["q_glob"], dev["q_loc"], dev["w_o"], dev["z_off"])
     torch.cuda.synchronize()
+    assert int(st.status.item()) == 0
 
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     with ClockSampler() as clock:
         t_wall = time.perf_counter()
         for k in range(args.steps):
             e = ev[k]
             e[0].record(stream)
-            st.attend(dev["kv"], dev["q_glob"], dev["q_loc"])
+            st.attend(prot_d, n_d, dev["kv"], dev["q_glob"], dev["q_loc"])
             e[1].record(stream)
-            st.merge()
+            st.oproj(prot_d, n_d, dev["w_o"], dev["z_off"])
             e[2].record(stream)
-            st.oproj(dev["w_o"], dev["z_off"])
-            e[3].record(stream)
         torch.cuda.synchronize()
         t_wall = time.perf_counter() - t_wall
     t_att = np.median([e[0].elapsed_time(e[1]) for e in ev]) / 1e3
-    t_mrg = np.median([e[1].elapsed_time(e[2]) for e in ev]) / 1e3
-    t_opj = np.median([e[2].elapsed_time(e[3]) for e in ev]) / 1e3
-    t_step = np.median([e[0].elapsed_time(e[3]) for e in ev]) / 1e3
+    t_opj = np.median([e[1].elapsed_time(e[2]) for e in ev]) / 1e3
+    t_step = np.median([e[0].elapsed_time(e[2]) for e in ev]) / 1e3
 
     value = (flop_attn + flop_oproj) / t_step / 1e12
     att_tflops = flop_attn / t_att / 1e12
-    merge_bytes = st.n_parts * (4 * g.d_latent + 4) + st.n_slots * (2 * g.d_latent + 4)
     oproj_bytes = (wl.n_rows - wl.n_prot) * g.d_model * 2 + wl.n_rows * g.d_model * 4 + head_rows * g.d_latent * 2
     out = {
         "metric": METRIC,
@@ -575,22 +613,44 @@ def main():
                    "segments": int(wl.segs.shape[0]), "heads": g.n_heads, "groups": g.n_groups,
                    "protected_rows": wl.n_prot, "d_latent": g.d_latent, "d_rope": g.d_rope,
                    "d_model": g.d_model, "proj_groups": g.n_proj_groups, "split_keys": split,
-                   "partials": st.n_parts},
+                   "prot_cap": prot_cap, "max_items": int(st.info.max_items),
+                   "path": "mla_online_plan once; per step mla_online_attend_planned (merge in the attention "
+                           "kernel, bf16 head outputs) + mla_sliced_oproj_add_planned (f32 z)"},
         "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "merged_rows_per_s": round(wl.n_rows / t_step, 1),
         "flop_attn": flop_attn,
         "flop_oproj": flop_oproj,
-        "ms": {"attend": round(t_att * 1e3, 3), "merge": round(t_mrg * 1e3, 3), "oproj": round(t_opj * 1e3, 3),
+        "ms": {"attend": round(t_att * 1e3, 3), "oproj": round(t_opj * 1e3, 3),
                "wall_per_step": round(t_wall / args.steps * 1e3, 3), "upload_s": round(t_upload, 2)},
-        "hbm_gbs": {"merge": round(merge_bytes / t_mrg / 1e9, 1), "oproj_add": round(oproj_bytes / t_opj / 1e9, 1)},
+        "hbm_gbs": {"oproj_add": round(oproj_bytes / t_opj / 1e9, 1)},
         "roofline": {"bound": "mfma", "achieved": round(att_tflops, 3), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4), "traffic": profiled_traffic(),
-                     "kernel": "attend_kernel<512,64> (timed with the plan kernels of mla_online_attend)"},
+                     "kernel": "attend_kernel<512,64> (timed with the device plan kernels of "
+                               "mla_online_attend_planned)"},
     }
     out["clock"] = clock.report()
-    out["dense_oproj"] = dense_oproj(wl, st, dev, torch, stream)
+    # the step's z in bf16 (the hand-off to W_b), then W_b on it
+    from paper_2609_07008_amd import mla
+    z16 = torch.empty((wl.n_rows, g.d_model), dtype=torch.bfloat16, device="cuda")
+    n_glob = wl.n_rows * g.n_groups
+    ts = []
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        mla.sliced_oproj_add_planned(g, st.info, st.out_o[:n_glob], st.out_o[n_glob:], wl.glob_head, prot_d, n_d,
+                                     dev["w_o"], dev["z_off"], z16, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ms16 = float(np.median(ts[1:]))
+    b16 = (wl.n_rows - wl.n_prot) * g.d_model * 2 + wl.n_rows * g.d_model * 2 + head_rows * g.d_latent * 2
+    out["oproj_bf16_z"] = {"ms": round(ms16, 3), "GB_per_s": round(b16 / (ms16 * 1e-3) / 1e9, 1)}
+    out["shared_wb"] = shared_wb_bench(torch, stream, z16)
+    del z16
+    out["dense_oproj"] = dense_oproj(wl, st.out_o, dev, torch, stream)
     del st
     torch.cuda.empty_cache()
+    out["host_plan_step"] = host_plan_step(wl, dev, torch, stream, split)
     if not args.no_rotary_value:
         out["rotary_value"] = rotary_value_step(wl, dev, torch, stream, split)
     del dev
@@ -601,7 +661,6 @@ def main():
         out["offline_producer"] = offline_producer(wl, torch, stream)
     out["protected_set"] = protected_set(wl, torch, stream)
     out["moe_fanout"] = moe_fanout_bench(torch, stream, wl.n_rows)
-    out["shared_wb"] = shared_wb_bench(torch, stream, wl.n_rows)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
     print(json.dumps(out), flush=True)

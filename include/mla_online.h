@@ -217,6 +217,101 @@ mla_status mla_sliced_oproj_add(const mla_geom* geom, int64_t n_rows, const void
                                 const void* z_off, float* z, void* stream);
 
 /* ----------------------------------------------------------------------------
+ * Plan once, then attend with the protected set in device memory.
+ *
+ * In a serving loop the segment table is fixed for a request, while the
+ * protected set A is recomputed in every layer on the device (Alg. 2:
+ * ProtectedRows, then SelectiveMLA in the same layer; eq:protected).  The
+ * calls below split the step accordingly:
+ *   mla_online_plan_query  host only: sizes of the plan image and workspace;
+ *   mla_online_plan        once per request: builds, on the host, everything
+ *                          that depends only on the segment table and uploads it
+ *                          into the caller's `plan` buffer (this call stages the
+ *                          image through the library's pinned buffer like
+ *                          mla_online_attend, so it is not capturable);
+ *   mla_online_attend_planned, mla_sliced_oproj_add_planned
+ *                          every layer: take prot_rows and |A| from device
+ *                          memory, enqueue kernels only (no copy, no memset, no
+ *                          host synchronization), and may be captured in a HIP
+ *                          graph.  The plan buffer is only read, so any number
+ *                          of calls (layers, streams) may share it.
+ * prot_cap is the largest |A| the plan accepts; outputs are sized for it.
+ * ------------------------------------------------------------------------- */
+typedef struct mla_plan_info {
+  mla_geom geom;          /* the geometry the plan was built for                          */
+  int64_t n_rows;         /* N                                                            */
+  int64_t split_keys;     /* chunking, as for mla_online_attend                           */
+  int64_t max_slots;      /* N*G + prot_cap*L_h: rows out_o must hold                     */
+  int64_t max_parts;      /* largest number of partials of one call (part_seg rows)       */
+  int32_t n_segs;
+  int32_t prot_cap;       /* largest |A| accepted                                         */
+  int32_t max_items;      /* largest number of attention work items of one call           */
+  int32_t one_chunk;      /* 1: one chunk per slot, the merge is done inside the attention */
+  size_t plan_bytes;      /* device bytes of the plan image                               */
+  size_t ws_bytes;        /* device workspace bytes of mla_online_attend_planned          */
+  int64_t layout[24];     /* offsets of the plan's and the workspace's tables (library use) */
+  uint64_t check;         /* checksum of the fields above, set by the library             */
+} mla_plan_info;
+
+/* Sizes only (host, pure): fills *info for the geometry, segment table (as for
+ * mla_online_attend), split_keys >= 0 and 0 <= prot_cap <= N.
+ * Errors: NULL, SHAPE, UNSUPPORTED, SEGMENTS. */
+mla_status mla_online_plan_query(const mla_geom* geom, const mla_segment* segs, int32_t n_segs,
+                                 int64_t split_keys, int32_t prot_cap, mla_plan_info* info);
+
+/* Builds the plan: fills *info as the query does and writes the plan image
+ * (info->plan_bytes) into `plan` (device, 256-byte aligned) on `stream`.
+ * Errors: as for the query, and WORKSPACE (plan_bytes too small), HIP. */
+mla_status mla_online_plan(const mla_geom* geom, const mla_segment* segs, int32_t n_segs, int64_t split_keys,
+                           int32_t prot_cap, mla_plan_info* info, void* plan, size_t plan_bytes, void* stream);
+
+/* Steps 1-3 with the protected set in device memory (Alg. 2: SelectiveMLA with
+ * the query relocated per segment, and SegmentedLSEMerge): the merged head output
+ * and lse of every slot, slot order as for mla_online_attend with the slots of
+ * protected row a following prot_rows[a].  With one chunk per slot the merge is
+ * the attention kernel's own online rescaling; otherwise the partials live in the
+ * workspace and a merge kernel follows in the same call.
+ *  geom, info, plan  the geometry (must equal info->geom), and a plan built by
+ *                    mla_online_plan (host description and device image)
+ *  prot_rows  device int32 [prot_cap]: strictly increasing storage rows; the
+ *             first *n_prot are used
+ *  n_prot     device int32 [1]: |A|
+ *  kv, q_glob as for mla_online_attend; q_loc device bf16 [prot_cap, G, hpg-1, D]
+ *             (the first *n_prot rows are read; NULL when hpg == 1)
+ *  out_dtype  MLA_BF16 or MLA_F32: element type of out_o
+ *  out_o      device [info->max_slots, d_v]: rows [0, N*G + |A|*L_h) written
+ *  out_lse    device f32 [info->max_slots] or NULL: natural-log lse of each slot
+ *  part_ptr   device i64 [info->max_slots + 1] or NULL: CSR offsets of each slot's
+ *             partials (entries [0, n_slots] written)
+ *  part_seg   device i32 [info->max_parts, 2] or NULL (needs part_ptr): first and
+ *             last segment of each partial
+ *  row_src    device u8 [N] or NULL: 1 on protected rows
+ *  status     device int32 [1] or NULL: MLA_OK, or MLA_ERR_ROWS when the device
+ *             list was rejected (|A| > prot_cap or < 0, a row outside [0, N), not
+ *             strictly increasing); the call then writes no output row
+ *  workspace  device, 256-byte aligned, info->ws_bytes; overwritten
+ * Host errors (nothing enqueued): NULL, SHAPE (also a geometry or info that does
+ * not match), WORKSPACE, HIP. */
+mla_status mla_online_attend_planned(const mla_geom* geom, const mla_plan_info* info, const void* plan,
+                                     const int32_t* prot_rows, const int32_t* n_prot, const void* kv,
+                                     const void* q_glob, const void* q_loc, int32_t out_dtype, void* out_o,
+                                     float* out_lse, int64_t* part_ptr, int32_t* part_seg, uint8_t* row_src,
+                                     int32_t* status, void* workspace, size_t ws_bytes, void* stream);
+
+/* Step 4 with the protected set in device memory: as mla_sliced_oproj_add, with
+ * |A| read from the device (clamped to [0, info->prot_cap]) and z in f32 or bf16.
+ *  o_glob, o_loc  the first N*G rows of out_o and the rows after them
+ *  prot_rows, n_prot  as for mla_online_attend_planned (entries outside [0, N)
+ *             are skipped by the Local pass, as in mla_sliced_oproj_add)
+ *  z_dtype    MLA_F32 or MLA_BF16 (the latter is what mla_shared_wb takes; a
+ *             protected row then carries the rounding of its Local sum and of z)
+ * Errors: NULL, SHAPE, UNSUPPORTED, HIP. */
+mla_status mla_sliced_oproj_add_planned(const mla_geom* geom, const mla_plan_info* info, const void* o_glob,
+                                        const void* o_loc, const int32_t* glob_head, const int32_t* prot_rows,
+                                        const int32_t* n_prot, const void* w_o, const void* z_off, int32_t z_dtype,
+                                        void* z, void* stream);
+
+/* ----------------------------------------------------------------------------
  * mla_offline_produce -- the MLA-Off native producer (Alg. 1, NativeProducer;
  * eq:offonline): the Local-head artifact of every row of every segment,
  *   z_off[r] = sum_{h Local} W_block(h)^T O_h^can[r],

@@ -125,6 +125,73 @@ struct Plan {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// What depends only on the segment table: request order, storage order, the
+// chunking of each segment's visible list (ranks 0 .. rank(s)) and the Global
+// partial index.  offline: every segment sees only itself (Alg. 1).
+struct SegTables {
+  std::vector<int32_t> rank_seg, storage, rank_of;
+  std::vector<mla::SegInfo> info;
+  std::vector<mla::ChunkInfo> chunks;
+  int64_t global_parts = 0;
+};
+
+void segment_tables(const mla_geom* g, const mla_segment* segs, int32_t n_segs, int64_t split_keys, bool offline,
+                    SegTables* T) {
+  const int G = g->n_groups;
+  T->rank_seg.resize(n_segs);
+  T->storage.resize(n_segs);
+  T->rank_of.resize(n_segs);
+  std::iota(T->rank_seg.begin(), T->rank_seg.end(), 0);
+  std::sort(T->rank_seg.begin(), T->rank_seg.end(),
+            [&](int32_t x, int32_t y) { return segs[x].req_offset < segs[y].req_offset; });
+  for (int32_t r = 0; r < n_segs; ++r) T->rank_of[T->rank_seg[r]] = r;
+  std::iota(T->storage.begin(), T->storage.end(), 0);
+  std::sort(T->storage.begin(), T->storage.end(),
+            [&](int32_t x, int32_t y) { return segs[x].kv_start < segs[y].kv_start; });
+  T->info.assign(n_segs, mla::SegInfo{});
+  T->chunks.clear();
+  for (int32_t s = 0; s < n_segs; ++s) {
+    mla::SegInfo& in = T->info[s];
+    in.kv_start = segs[s].kv_start;
+    in.length = segs[s].length;
+    in.req_offset = segs[s].req_offset;
+    in.rank = T->rank_of[s];
+    in.chunk_off = (int32_t)T->chunks.size();
+    if (offline) {
+      T->chunks.push_back({T->rank_of[s], T->rank_of[s]});
+      in.n_chunks = 1;
+      continue;
+    }
+    int32_t first = 0;
+    int64_t keys = 0;
+    for (int32_t r = 0; r <= T->rank_of[s]; ++r) {
+      const int64_t len = segs[T->rank_seg[r]].length;
+      const bool close = split_keys == 0 ? (r > first) : (r > first && keys + len > split_keys);
+      if (close) {
+        T->chunks.push_back({first, r - 1});
+        first = r;
+        keys = 0;
+      }
+      keys += len;
+    }
+    T->chunks.push_back({first, T->rank_of[s]});
+    in.n_chunks = (int32_t)T->chunks.size() - in.chunk_off;
+  }
+  // partial counts: global slots in storage order (none offline)
+  int64_t cum = 0;
+  for (int32_t i : T->storage) {
+    T->info[i].cum_global = cum;
+    if (!offline) cum += (int64_t)G * T->info[i].length * T->info[i].n_chunks;
+  }
+  T->global_parts = cum;
+}
+
+// RoPE frequencies in revolutions: base^(-2j/d_r) / (2 pi)
+void rope_theta_rev(const mla_geom* g, double* th) {
+  const double two_pi = 6.283185307179586476925286766559;
+  for (int j = 0; j < g->d_rope / 2; ++j) th[j] = std::pow(g->rope_base, -2.0 * j / g->d_rope) / two_pi;
+}
+
 // offline: the producer's plan (Alg. 1) -- every segment sees only itself, and
 // only Local heads run (every row is listed in prot, no Global slots exist).
 mla_status build_plan(const mla_geom* g, const mla_segment* segs, int32_t n_segs, const int32_t* prot,
@@ -138,54 +205,13 @@ mla_status build_plan(const mla_geom* g, const mla_segment* segs, int32_t n_segs
 
   const int G = g->n_groups, hpg = g->n_heads / g->n_groups;
   const int64_t Lh = (int64_t)G * (hpg - 1);
-
-  // request order and storage order
-  std::vector<int32_t> rank_seg(n_segs), storage(n_segs), rank_of(n_segs);
-  std::iota(rank_seg.begin(), rank_seg.end(), 0);
-  std::sort(rank_seg.begin(), rank_seg.end(),
-            [&](int32_t x, int32_t y) { return segs[x].req_offset < segs[y].req_offset; });
-  for (int32_t r = 0; r < n_segs; ++r) rank_of[rank_seg[r]] = r;
-  std::iota(storage.begin(), storage.end(), 0);
-  std::sort(storage.begin(), storage.end(),
-            [&](int32_t x, int32_t y) { return segs[x].kv_start < segs[y].kv_start; });
-
-  // chunks of each segment's visible list (ranks 0 .. rank(s))
-  std::vector<mla::SegInfo> info(n_segs);
-  std::vector<mla::ChunkInfo> chunks;
-  for (int32_t s = 0; s < n_segs; ++s) {
-    info[s].kv_start = segs[s].kv_start;
-    info[s].length = segs[s].length;
-    info[s].req_offset = segs[s].req_offset;
-    info[s].rank = rank_of[s];
-    info[s].chunk_off = (int32_t)chunks.size();
-    if (offline) {
-      chunks.push_back({rank_of[s], rank_of[s]});
-      info[s].n_chunks = 1;
-      continue;
-    }
-    int32_t first = 0;
-    int64_t keys = 0;
-    for (int32_t r = 0; r <= rank_of[s]; ++r) {
-      const int64_t len = segs[rank_seg[r]].length;
-      const bool close = split_keys == 0 ? (r > first) : (r > first && keys + len > split_keys);
-      if (close) {
-        chunks.push_back({first, r - 1});
-        first = r;
-        keys = 0;
-      }
-      keys += len;
-    }
-    chunks.push_back({first, rank_of[s]});
-    info[s].n_chunks = (int32_t)chunks.size() - info[s].chunk_off;
-  }
-
-  // partial counts: global slots in storage order, then local slots
-  int64_t cum = 0;
-  for (int32_t i : storage) {
-    info[i].cum_global = cum;
-    if (!offline) cum += (int64_t)G * info[i].length * info[i].n_chunks;
-  }
-  const int64_t global_parts = cum;
+  SegTables T;
+  segment_tables(g, segs, n_segs, split_keys, offline, &T);
+  const std::vector<int32_t>& rank_seg = T.rank_seg;
+  const std::vector<int32_t>& storage = T.storage;
+  std::vector<mla::SegInfo>& info = T.info;
+  const std::vector<mla::ChunkInfo>& chunks = T.chunks;
+  const int64_t global_parts = T.global_parts;
   std::vector<int32_t> prot_seg(n_prot);
   std::vector<int64_t> cum_local(n_prot + 1, 0);
   {
@@ -290,11 +316,29 @@ mla_status build_plan(const mla_geom* g, const mla_segment* segs, int32_t n_segs
     std::memcpy(B + h.off_prot_seg, prot_seg.data(), sizeof(int32_t) * n_prot);
   }
   std::memcpy(B + h.off_cum_local, cum_local.data(), sizeof(int64_t) * (n_prot + 1));
-  double* th = reinterpret_cast<double*>(B + h.off_theta);
-  const double two_pi = 6.283185307179586476925286766559;
-  for (int j = 0; j < g->d_rope / 2; ++j)
-    th[j] = std::pow(g->rope_base, -2.0 * j / g->d_rope) / two_pi;
+  rope_theta_rev(g, reinterpret_cast<double*>(B + h.off_theta));
   return MLA_OK;
+}
+
+// device pointers of a host plan's tables inside the workspace it was uploaded to
+void host_plan_tables(mla::AttendArgs& a, const mla::PlanHeader& h, const unsigned char* ws) {
+  a.segs = reinterpret_cast<const mla::SegInfo*>(ws + h.off_segs);
+  a.rank_seg = reinterpret_cast<const int32_t*>(ws + h.off_rank);
+  a.storage = reinterpret_cast<const int32_t*>(ws + h.off_storage);
+  a.chunks = reinterpret_cast<const mla::ChunkInfo*>(ws + h.off_chunks);
+  a.items = reinterpret_cast<const mla::WorkItem*>(ws + h.off_items);
+  a.prot = reinterpret_cast<const int32_t*>(ws + h.off_prot);
+  a.theta_rev = reinterpret_cast<const double*>(ws + h.off_theta);
+  a.prot_seg = reinterpret_cast<const int32_t*>(ws + h.off_prot_seg);
+  a.cum_local = reinterpret_cast<const int64_t*>(ws + h.off_cum_local);
+  a.dyn = nullptr;
+  a.n_rows = h.n_rows;
+  a.n_slots = h.n_slots;
+  a.n_parts = h.n_parts;
+  a.global_parts = h.global_parts;
+  a.n_items = h.n_items;
+  a.n_prot = h.n_prot;
+  a.n_segs = h.n_segs;
 }
 
 // ---------------------------------------------------------------------------
@@ -420,11 +464,7 @@ mla_status mla_online_attend(const mla_geom* geom, const mla_segment* segs, int3
   a.part_ptr = part_ptr;
   a.part_seg = part_seg;
   a.row_src = row_src;
-  a.ws = reinterpret_cast<const unsigned char*>(workspace);
-  a.n_rows = p.hdr.n_rows;
-  a.n_slots = p.hdr.n_slots;
-  a.n_items = p.hdr.n_items;
-  a.n_prot = n_prot;
+  host_plan_tables(a, p.hdr, reinterpret_cast<const unsigned char*>(workspace));
   a.n_groups = geom->n_groups;
   a.n_local = geom->n_groups * (hpg - 1);
   a.d_latent = geom->d_latent;
@@ -432,8 +472,7 @@ mla_status mla_online_attend(const mla_geom* geom, const mla_segment* segs, int3
   a.dv = head_dv(geom);
   a.scale_log2 = geom->softmax_scale * 1.4426950408889634f;
   a.local_slot_base = p.hdr.n_rows * geom->n_groups;
-  a.out_bf16 = nullptr;
-  a.hdr = p.hdr;
+  a.out_direct = nullptr;
   hipError_t e = mla::launch_plan(a, s);
   if (e != hipSuccess) return hip_fail(e, "plan kernels");
   e = mla::launch_attend(a, s);
@@ -499,6 +538,362 @@ mla_status mla_sliced_oproj_add(const mla_geom* geom, int64_t n_rows, const void
   for (int g = 0; g < geom->n_groups; ++g) a.glob_head[g] = glob_head[g];
   a.z_bf16 = 0;
   hipError_t e = mla::launch_oproj(a, 3, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "o-proj kernels");
+  return MLA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// plan once per request; attend and project with the protected set on the device
+// ---------------------------------------------------------------------------
+namespace {
+
+// indices into mla_plan_info::layout: byte offsets in the plan image (P_*) and
+// in the workspace (W_*), and two counts
+enum {
+  P_SEGS, P_RANK, P_STORAGE, P_CHUNKS, P_THETA, P_GROUPS, N_ITEM_GROUPS, GLOBAL_PARTS,
+  W_DYN, W_SEG_LO, W_SEG_CNT, W_SEG_BASE, W_GROUP_BASE, W_ITEMS, W_PART_PTR, W_PART_O, W_PART_LSE, W_LSE,
+  LAYOUT_USED
+};
+static_assert(LAYOUT_USED <= 24, "mla_plan_info::layout holds 24 entries");
+
+uint64_t mix(uint64_t h, uint64_t v) {
+  for (int i = 0; i < 8; ++i) {   // FNV-1a over the little-endian bytes of v
+    h ^= (v >> (8 * i)) & 0xffu;
+    h *= 1099511628211ull;
+  }
+  return h;
+}
+
+uint64_t info_checksum(const mla_plan_info* p) {
+  uint64_t h = 1469598103934665603ull;
+  const mla_geom& g = p->geom;
+  const int64_t gv[] = {g.n_heads, g.n_groups, g.d_latent, g.d_rope, g.d_model, g.n_proj_groups, g.value_rope};
+  for (int64_t v : gv) h = mix(h, (uint64_t)v);
+  uint32_t sc;
+  std::memcpy(&sc, &g.softmax_scale, 4);
+  uint64_t rb;
+  std::memcpy(&rb, &g.rope_base, 8);
+  h = mix(mix(h, sc), rb);
+  const int64_t v[] = {p->n_rows, p->split_keys, p->max_slots, p->max_parts, p->n_segs, p->prot_cap,
+                       p->max_items, p->one_chunk, (int64_t)p->plan_bytes, (int64_t)p->ws_bytes};
+  for (int64_t x : v) h = mix(h, (uint64_t)x);
+  for (int i = 0; i < 24; ++i) h = mix(h, (uint64_t)p->layout[i]);
+  return h;
+}
+
+bool same_geom(const mla_geom& a, const mla_geom& b) {
+  return a.n_heads == b.n_heads && a.n_groups == b.n_groups && a.d_latent == b.d_latent && a.d_rope == b.d_rope &&
+         a.d_model == b.d_model && a.n_proj_groups == b.n_proj_groups && a.value_rope == b.value_rope &&
+         std::memcmp(&a.softmax_scale, &b.softmax_scale, 4) == 0 && std::memcmp(&a.rope_base, &b.rope_base, 8) == 0;
+}
+
+struct StaticPlan {
+  SegTables T;
+  std::vector<mla::ItemGroup> groups;
+  std::vector<unsigned char> blob;
+};
+
+// The static plan and its sizes.  Item groups: one per (kind, segment, chunk),
+// in launch order: largest upper bound of an item's cost first (the chunk's
+// key tiles with the segment's own keys all visible), stable.
+mla_status static_plan(const mla_geom* g, const mla_segment* segs, int32_t n_segs, int64_t split_keys,
+                       int32_t prot_cap, bool want_blob, mla_plan_info* info, StaticPlan* out) {
+  if (info == nullptr) return fail(MLA_ERR_NULL, "info is NULL");
+  mla_status st = check_geom(g, false);
+  if (st != MLA_OK) return st;
+  int64_t N = 0;
+  if ((st = check_segments(segs, n_segs, &N)) != MLA_OK) return st;
+  if (split_keys < 0) return fail(MLA_ERR_SHAPE, "split_keys = %lld must be >= 0", (long long)split_keys);
+  if (prot_cap < 0 || prot_cap > N) return fail(MLA_ERR_SHAPE, "prot_cap = %d outside [0, %lld]", prot_cap, (long long)N);
+  const int G = g->n_groups, hpg = g->n_heads / g->n_groups;
+  const int64_t Lh = (int64_t)G * (hpg - 1);
+  SegTables& T = out->T;
+  segment_tables(g, segs, n_segs, split_keys, false, &T);
+
+  struct Cand {
+    mla::ItemGroup grp;
+    int64_t ub;
+  };
+  std::vector<Cand> cands;
+  int64_t global_items = 0, local_terms = 0;
+  int32_t max_chunks = 0;
+  for (int32_t s = 0; s < n_segs; ++s) {
+    const mla::SegInfo& in = T.info[s];
+    max_chunks = std::max(max_chunks, in.n_chunks);
+    for (int32_t c = 0; c < in.n_chunks; ++c) {
+      const mla::ChunkInfo ch = T.chunks[in.chunk_off + c];
+      int64_t tiles = 0;
+      for (int32_t r = ch.first_rank; r <= ch.last_rank; ++r) tiles += (segs[T.rank_seg[r]].length + 63) / 64;
+      const int64_t n_glob = (in.length * G + mla::kTileRows - 1) / mla::kTileRows;
+      cands.push_back({{0, s, c, (int32_t)n_glob}, tiles});
+      global_items += n_glob;
+      if (Lh > 0) {
+        cands.push_back({{1, s, c, 0}, tiles});
+        ++local_terms;
+      }
+    }
+  }
+  std::stable_sort(cands.begin(), cands.end(), [](const Cand& x, const Cand& y) { return x.ub > y.ub; });
+  out->groups.resize(cands.size());
+  for (size_t i = 0; i < cands.size(); ++i) out->groups[i] = cands[i].grp;
+
+  // bounds over every protected set of at most prot_cap rows: the most
+  // chunk-weighted placement fills the segments with the most chunks first
+  int64_t weighted = 0;   // max over A of sum_a n_chunks(seg(a))
+  if (Lh > 0) {
+    std::vector<int32_t> by_chunks(T.storage);
+    std::stable_sort(by_chunks.begin(), by_chunks.end(),
+                     [&](int32_t x, int32_t y) { return T.info[x].n_chunks > T.info[y].n_chunks; });
+    int64_t left = prot_cap;
+    for (int32_t sidx : by_chunks) {
+      const int64_t take = std::min<int64_t>(left, T.info[sidx].length);
+      weighted += take * T.info[sidx].n_chunks;
+      left -= take;
+      if (left == 0) break;
+    }
+  }
+  const int64_t local_items = Lh > 0 ? weighted * Lh / mla::kTileRows + local_terms : 0;
+  if (global_items + local_items > (int64_t)INT32_MAX - 256)
+    return fail(MLA_ERR_UNSUPPORTED, "too many work items for one launch");
+
+  std::memset(info, 0, sizeof *info);
+  info->geom = *g;
+  info->n_rows = N;
+  info->split_keys = split_keys;
+  info->max_slots = N * G + (int64_t)prot_cap * Lh;
+  info->max_parts = T.global_parts + weighted * Lh;
+  info->n_segs = n_segs;
+  info->prot_cap = prot_cap;
+  info->max_items = (int32_t)(global_items + local_items);
+  info->one_chunk = max_chunks == 1 ? 1 : 0;
+  int64_t* L = info->layout;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, 256);
+    return (int64_t)o;
+  };
+  L[P_SEGS] = take(sizeof(mla::SegInfo) * n_segs);
+  L[P_RANK] = take(sizeof(int32_t) * n_segs);
+  L[P_STORAGE] = take(sizeof(int32_t) * n_segs);
+  L[P_CHUNKS] = take(sizeof(mla::ChunkInfo) * T.chunks.size());
+  L[P_THETA] = take(sizeof(double) * mla::kMaxRopePairs);
+  L[P_GROUPS] = take(sizeof(mla::ItemGroup) * std::max<size_t>(out->groups.size(), 1));
+  L[N_ITEM_GROUPS] = (int64_t)out->groups.size();
+  L[GLOBAL_PARTS] = T.global_parts;
+  info->plan_bytes = off;
+  off = 0;
+  const int dv = head_dv(g);
+  L[W_DYN] = take(sizeof(mla::DynPlan));
+  L[W_SEG_LO] = take(sizeof(int32_t) * n_segs);
+  L[W_SEG_CNT] = take(sizeof(int32_t) * n_segs);
+  L[W_SEG_BASE] = take(sizeof(int64_t) * n_segs);
+  L[W_GROUP_BASE] = take(sizeof(int32_t) * (out->groups.size() + 1));
+  L[W_ITEMS] = take(sizeof(mla::WorkItem) * std::max<int64_t>(info->max_items, 1));
+  if (info->one_chunk) {
+    L[W_PART_PTR] = L[W_PART_O] = L[W_PART_LSE] = -1;
+    L[W_LSE] = g->value_rope ? take(sizeof(float) * (size_t)info->max_slots) : -1;
+  } else {
+    L[W_PART_PTR] = take(sizeof(int64_t) * (size_t)(info->max_slots + 1));
+    L[W_PART_O] = take(sizeof(float) * (size_t)info->max_parts * dv);
+    L[W_PART_LSE] = take(sizeof(float) * (size_t)info->max_parts);
+    L[W_LSE] = -1;
+  }
+  info->ws_bytes = off;
+  info->check = info_checksum(info);
+  if (!want_blob) return MLA_OK;
+
+  out->blob.assign(info->plan_bytes, 0);
+  unsigned char* B = out->blob.data();
+  std::memcpy(B + L[P_SEGS], T.info.data(), sizeof(mla::SegInfo) * n_segs);
+  std::memcpy(B + L[P_RANK], T.rank_seg.data(), sizeof(int32_t) * n_segs);
+  std::memcpy(B + L[P_STORAGE], T.storage.data(), sizeof(int32_t) * n_segs);
+  std::memcpy(B + L[P_CHUNKS], T.chunks.data(), sizeof(mla::ChunkInfo) * T.chunks.size());
+  rope_theta_rev(g, reinterpret_cast<double*>(B + L[P_THETA]));
+  if (!out->groups.empty())
+    std::memcpy(B + L[P_GROUPS], out->groups.data(), sizeof(mla::ItemGroup) * out->groups.size());
+  return MLA_OK;
+}
+
+// the checks shared by the two planned calls
+mla_status check_planned(const mla_geom* geom, const mla_plan_info* info) {
+  if (geom == nullptr || info == nullptr) return fail(MLA_ERR_NULL, "geom and info are required");
+  if (info->check != info_checksum(info))
+    return fail(MLA_ERR_SHAPE, "info was not written by mla_online_plan (or was changed since)");
+  if (!same_geom(*geom, info->geom)) return fail(MLA_ERR_SHAPE, "geom differs from the geometry of the plan");
+  return check_geom(geom, false);
+}
+
+}  // namespace
+
+mla_status mla_online_plan_query(const mla_geom* geom, const mla_segment* segs, int32_t n_segs, int64_t split_keys,
+                                 int32_t prot_cap, mla_plan_info* info) {
+  g_detail.clear();
+  StaticPlan sp;
+  return static_plan(geom, segs, n_segs, split_keys, prot_cap, false, info, &sp);
+}
+
+mla_status mla_online_plan(const mla_geom* geom, const mla_segment* segs, int32_t n_segs, int64_t split_keys,
+                           int32_t prot_cap, mla_plan_info* info, void* plan, size_t plan_bytes, void* stream) {
+  g_detail.clear();
+  StaticPlan sp;
+  mla_status st = static_plan(geom, segs, n_segs, split_keys, prot_cap, true, info, &sp);
+  if (st != MLA_OK) return st;
+  if (plan == nullptr) return fail(MLA_ERR_NULL, "plan is NULL");
+  if ((reinterpret_cast<uintptr_t>(plan) & 255u) != 0) return fail(MLA_ERR_SHAPE, "plan must be 256-byte aligned");
+  if (plan_bytes < info->plan_bytes)
+    return fail(MLA_ERR_WORKSPACE, "plan buffer %zu bytes < required %zu", plan_bytes, info->plan_bytes);
+  Plan p;
+  p.blob = std::move(sp.blob);
+  return upload_plan(p, plan, reinterpret_cast<hipStream_t>(stream));
+}
+
+mla_status mla_online_attend_planned(const mla_geom* geom, const mla_plan_info* info, const void* plan,
+                                     const int32_t* prot_rows, const int32_t* n_prot, const void* kv,
+                                     const void* q_glob, const void* q_loc, int32_t out_dtype, void* out_o,
+                                     float* out_lse, int64_t* part_ptr, int32_t* part_seg, uint8_t* row_src,
+                                     int32_t* status, void* workspace, size_t ws_bytes, void* stream) {
+  g_detail.clear();
+  mla_status st = check_planned(geom, info);
+  if (st != MLA_OK) return st;
+  const int G = geom->n_groups, hpg = geom->n_heads / geom->n_groups;
+  const int64_t* L = info->layout;
+  if (plan == nullptr || n_prot == nullptr || kv == nullptr || q_glob == nullptr || out_o == nullptr ||
+      workspace == nullptr)
+    return fail(MLA_ERR_NULL, "plan, n_prot, kv, q_glob, out_o and workspace are required");
+  if (info->prot_cap > 0 && prot_rows == nullptr) return fail(MLA_ERR_NULL, "prot_rows is NULL");
+  if (info->prot_cap > 0 && hpg > 1 && q_loc == nullptr) return fail(MLA_ERR_NULL, "q_loc is NULL but Local heads exist");
+  if (part_seg != nullptr && part_ptr == nullptr) return fail(MLA_ERR_NULL, "part_seg needs part_ptr");
+  if (out_dtype != MLA_BF16 && out_dtype != MLA_F32) return fail(MLA_ERR_SHAPE, "out_dtype %d", out_dtype);
+  if (!aligned16(kv) || !aligned16(q_glob) || (q_loc && !aligned16(q_loc)) || !aligned16(out_o))
+    return fail(MLA_ERR_SHAPE, "kv, q_glob, q_loc and out_o must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 || (reinterpret_cast<uintptr_t>(plan) & 255u) != 0)
+    return fail(MLA_ERR_SHAPE, "plan and workspace must be 256-byte aligned");
+  if (ws_bytes < info->ws_bytes)
+    return fail(MLA_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, info->ws_bytes);
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const unsigned char* P = reinterpret_cast<const unsigned char*>(plan);
+  unsigned char* W = reinterpret_cast<unsigned char*>(workspace);
+  const int32_t n_local = G * (hpg - 1);
+
+  mla::DPlanArgs d{};
+  d.segs = reinterpret_cast<const mla::SegInfo*>(P + L[P_SEGS]);
+  d.storage = reinterpret_cast<const int32_t*>(P + L[P_STORAGE]);
+  d.groups = reinterpret_cast<const mla::ItemGroup*>(P + L[P_GROUPS]);
+  d.prot = prot_rows;
+  d.n_prot_dev = n_prot;
+  d.prot_cap = info->prot_cap;
+  d.n_rows = info->n_rows;
+  d.n_segs = info->n_segs;
+  d.n_item_groups = (int32_t)L[N_ITEM_GROUPS];
+  d.n_groups = G;
+  d.n_local = n_local;
+  d.global_parts = L[GLOBAL_PARTS];
+  d.max_parts = info->max_parts;
+  d.max_items = info->max_items;
+  d.dyn = reinterpret_cast<mla::DynPlan*>(W + L[W_DYN]);
+  d.seg_prot_lo = reinterpret_cast<int32_t*>(W + L[W_SEG_LO]);
+  d.seg_prot_cnt = reinterpret_cast<int32_t*>(W + L[W_SEG_CNT]);
+  d.seg_local_base = reinterpret_cast<int64_t*>(W + L[W_SEG_BASE]);
+  d.group_base = reinterpret_cast<int32_t*>(W + L[W_GROUP_BASE]);
+  d.items = reinterpret_cast<mla::WorkItem*>(W + L[W_ITEMS]);
+  d.status_out = status;
+  hipError_t e = mla::launch_dplan(d, s);
+  if (e != hipSuccess) return hip_fail(e, "plan kernels");
+
+  mla::AttendArgs a{};
+  a.kv = kv;
+  a.q_glob = q_glob;
+  a.q_loc = q_loc;
+  a.part_seg = part_seg;
+  a.row_src = row_src;
+  a.segs = d.segs;
+  a.rank_seg = reinterpret_cast<const int32_t*>(P + L[P_RANK]);
+  a.storage = d.storage;
+  a.chunks = reinterpret_cast<const mla::ChunkInfo*>(P + L[P_CHUNKS]);
+  a.items = d.items;
+  a.prot = prot_rows;
+  a.theta_rev = reinterpret_cast<const double*>(P + L[P_THETA]);
+  a.seg_prot_lo = d.seg_prot_lo;
+  a.seg_local_base = d.seg_local_base;
+  a.dyn = d.dyn;
+  a.n_rows = info->n_rows;
+  a.n_slots = info->max_slots;
+  a.n_parts = info->max_parts;
+  a.global_parts = L[GLOBAL_PARTS];
+  a.n_items = info->max_items;
+  a.n_prot = info->prot_cap;
+  a.n_segs = info->n_segs;
+  a.n_groups = G;
+  a.n_local = n_local;
+  a.d_latent = geom->d_latent;
+  a.d_rope = geom->d_rope;
+  a.dv = head_dv(geom);
+  a.scale_log2 = geom->softmax_scale * 1.4426950408889634f;
+  a.local_slot_base = info->n_rows * G;
+  if (info->one_chunk) {
+    a.part_ptr = part_ptr;
+    a.out_direct = out_o;
+    a.out_direct_bf16 = out_dtype == MLA_BF16 ? 1 : 0;
+    a.part_lse = out_lse != nullptr ? out_lse : (L[W_LSE] >= 0 ? reinterpret_cast<float*>(W + L[W_LSE]) : nullptr);
+  } else {
+    a.part_ptr = part_ptr != nullptr ? part_ptr : reinterpret_cast<int64_t*>(W + L[W_PART_PTR]);
+    a.part_o = reinterpret_cast<float*>(W + L[W_PART_O]);
+    a.part_lse = reinterpret_cast<float*>(W + L[W_PART_LSE]);
+  }
+  if ((e = mla::launch_plan(a, s)) != hipSuccess) return hip_fail(e, "plan kernels");
+  if ((e = mla::launch_attend(a, s)) != hipSuccess) return hip_fail(e, "attention kernel");
+  if (!info->one_chunk) {
+    e = mla::launch_merge(info->max_slots, a.dv, a.part_o, a.part_lse, a.part_ptr, out_dtype, out_o, out_lse, s,
+                          &d.dyn->n_slots);
+    if (e != hipSuccess) return hip_fail(e, "merge kernel");
+  }
+  return MLA_OK;
+}
+
+mla_status mla_sliced_oproj_add_planned(const mla_geom* geom, const mla_plan_info* info, const void* o_glob,
+                                        const void* o_loc, const int32_t* glob_head, const int32_t* prot_rows,
+                                        const int32_t* n_prot, const void* w_o, const void* z_off, int32_t z_dtype,
+                                        void* z, void* stream) {
+  g_detail.clear();
+  mla_status st = check_planned(geom, info);
+  if (st != MLA_OK) return st;
+  if ((st = check_geom(geom, true)) != MLA_OK) return st;
+  const int64_t N = info->n_rows;
+  const int hpg = geom->n_heads / geom->n_groups;
+  if (glob_head == nullptr) return fail(MLA_ERR_NULL, "glob_head is NULL");
+  for (int g = 0; g < geom->n_groups; ++g)
+    if (glob_head[g] < 0 || glob_head[g] >= hpg)
+      return fail(MLA_ERR_SHAPE, "glob_head[%d] = %d outside [0, %d)", g, glob_head[g], hpg);
+  if (o_glob == nullptr || w_o == nullptr || z == nullptr || z_off == nullptr || n_prot == nullptr)
+    return fail(MLA_ERR_NULL, "o_glob, w_o, z_off, z and n_prot are required");
+  if (info->prot_cap > 0 && prot_rows == nullptr) return fail(MLA_ERR_NULL, "prot_rows is NULL");
+  if (info->prot_cap > 0 && hpg > 1 && o_loc == nullptr) return fail(MLA_ERR_NULL, "o_loc is NULL but Local heads exist");
+  if (z_dtype != MLA_BF16 && z_dtype != MLA_F32) return fail(MLA_ERR_SHAPE, "z_dtype %d", z_dtype);
+  if (!aligned16(o_glob) || (o_loc && !aligned16(o_loc)) || !aligned16(w_o) || !aligned16(z) || !aligned16(z_off))
+    return fail(MLA_ERR_SHAPE, "o_glob, o_loc, w_o, z_off and z must be 16-byte aligned");
+  if (mla::oproj_workgroups(N, geom->d_model, geom->n_proj_groups) > INT32_MAX)
+    return fail(MLA_ERR_UNSUPPORTED, "%lld rows x d_model %d is more o-proj tiles than one launch takes",
+                (long long)N, geom->d_model);
+  mla::OprojArgs a{};
+  a.o_glob = o_glob;
+  a.o_loc = o_loc;
+  a.prot_rows = prot_rows;
+  a.w_o = w_o;
+  a.z_off = z_off;
+  a.z = reinterpret_cast<float*>(z);
+  a.n_rows = N;
+  a.n_prot = info->prot_cap;
+  a.n_prot_dev = n_prot;
+  a.n_heads = geom->n_heads;
+  a.n_groups = geom->n_groups;
+  a.d_latent = head_dv(geom);
+  a.d_model = geom->d_model;
+  a.n_pg = geom->n_proj_groups;
+  a.z_bf16 = z_dtype == MLA_BF16 ? 1 : 0;
+  for (int g = 0; g < geom->n_groups; ++g) a.glob_head[g] = glob_head[g];
+  const hipError_t e = mla::launch_oproj(a, 3, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "o-proj kernels");
   return MLA_OK;
 }
@@ -586,11 +981,7 @@ mla_status mla_offline_produce(const mla_geom* geom, const mla_segment* segs, in
   a.kv = kv;
   a.q_glob = q_loc;   // unused: the plan holds no Global items
   a.q_loc = q_loc;
-  a.ws = ws;
-  a.n_rows = N;
-  a.n_slots = L.plan.hdr.n_slots;
-  a.n_items = L.plan.hdr.n_items;
-  a.n_prot = (int32_t)N;
+  host_plan_tables(a, L.plan.hdr, ws);
   a.n_groups = geom->n_groups;
   a.n_local = geom->n_groups * (hpg - 1);
   a.d_latent = geom->d_latent;
@@ -598,9 +989,9 @@ mla_status mla_offline_produce(const mla_geom* geom, const mla_segment* segs, in
   a.dv = head_dv(geom);
   a.scale_log2 = geom->softmax_scale * 1.4426950408889634f;
   a.local_slot_base = 0;
-  a.out_bf16 = reinterpret_cast<uint16_t*>(ws + L.off_o);
+  a.out_direct = ws + L.off_o;
+  a.out_direct_bf16 = 1;
   a.part_lse = geom->value_rope ? reinterpret_cast<float*>(ws + L.off_lse) : nullptr;
-  a.hdr = L.plan.hdr;
   hipError_t e = mla::launch_attend(a, s);
   if (e != hipSuccess) return hip_fail(e, "attention kernel");
 

@@ -142,18 +142,21 @@ __device__ __forceinline__ int xcd_item_id(int b) {
   return (kx >> 5) * 256 + xcd * 32 + (kx & 31);
 }
 
+// work items of this launch: the host plan's count, or the device plan's
+__device__ __forceinline__ int item_count(const AttendArgs& a) {
+  return a.dyn != nullptr ? a.dyn->n_items : a.n_items;
+}
+
 template <class C>
 __device__ __forceinline__ ItemView item_view(const AttendArgs& a, int item_id, int wave, int l32) {
   ItemView v;
-  const unsigned char* ws = a.ws;
-  v.segs = (const SegInfo*)(ws + a.hdr.off_segs);
-  v.rank_seg = (const int32_t*)(ws + a.hdr.off_rank);
-  v.theta_rev = (const double*)(ws + a.hdr.off_theta);
-  const ChunkInfo* chunks = (const ChunkInfo*)(ws + a.hdr.off_chunks);
-  const int32_t* prot = (const int32_t*)(ws + a.hdr.off_prot);
-  v.it = ((const WorkItem*)(ws + a.hdr.off_items))[item_id];
+  v.segs = a.segs;
+  v.rank_seg = a.rank_seg;
+  v.theta_rev = a.theta_rev;
+  const int32_t* prot = a.prot;
+  v.it = a.items[item_id];
   v.own = v.segs[v.it.seg];
-  v.chk = chunks[v.own.chunk_off + v.it.chunk];
+  v.chk = a.chunks[v.own.chunk_off + v.it.chunk];
   const int hr_local = wave * 32 + l32;
   v.valid = hr_local < v.it.count;
   v.active = wave * 32 < v.it.count;
@@ -264,7 +267,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   const int half = lane >> 5, l32 = lane & 31;
 
   const int item_id = xcd_item_id(blockIdx.x);
-  if (item_id >= a.n_items) return;
+  if (item_id >= item_count(a)) return;
   const ItemView v = item_view<C>(a, item_id, wave, l32);
   const SegInfo* segs = v.segs;
   const int32_t* rank_seg = v.rank_seg;
@@ -575,17 +578,28 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   if (!valid) return;
   const float l_tot = lx + ly;
   const float inv = 1.f / l_tot;
-  if (a.out_bf16 != nullptr) {
-    // one chunk per slot (the offline producer): the head output itself, in bf16;
-    // with a rotary value its lse too (the rotary pass normalizes with it)
-    uint16_t* ob = a.out_bf16 + slot * a.dv;
+  if (a.out_direct != nullptr) {
+    // one chunk per slot (the merge done here by online rescaling, or the
+    // offline producer): the head output itself, and its lse when asked for (a
+    // rotary value's second pass normalizes with it)
     if (a.part_lse != nullptr && half == 0) a.part_lse[slot] = (m_run + __log2f(l_tot)) * 0.6931471805599453f;
+    if (a.out_direct_bf16) {
+      uint16_t* ob = (uint16_t*)a.out_direct + slot * a.dv;
 #pragma unroll
-    for (int d = 0; d < C::OB; ++d)
+      for (int d = 0; d < C::OB; ++d)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        *(u32x2*)(ob + d * 32 + half * 4 + 8 * i) = u32x2{pack_bf16x2(o[d][4 * i] * inv, o[d][4 * i + 1] * inv),
-                                                          pack_bf16x2(o[d][4 * i + 2] * inv, o[d][4 * i + 3] * inv)};
+        for (int i = 0; i < 4; ++i)
+          *(u32x2*)(ob + d * 32 + half * 4 + 8 * i) = u32x2{pack_bf16x2(o[d][4 * i] * inv, o[d][4 * i + 1] * inv),
+                                                            pack_bf16x2(o[d][4 * i + 2] * inv, o[d][4 * i + 3] * inv)};
+    } else {
+      float* of = (float*)a.out_direct + slot * a.dv;
+#pragma unroll
+      for (int d = 0; d < C::OB; ++d)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          *(f32x4*)(of + d * 32 + half * 4 + 8 * i) =
+              f32x4{o[d][4 * i] * inv, o[d][4 * i + 1] * inv, o[d][4 * i + 2] * inv, o[d][4 * i + 3] * inv};
+    }
     return;
   }
   const int64_t pidx = a.part_ptr[slot] + it.chunk;
@@ -624,7 +638,7 @@ __global__ __launch_bounds__(256, 1) void attend_vrope_kernel(AttendArgs a) {
   const int half = lane >> 5, l32 = lane & 31;
 
   const int item_id = xcd_item_id(blockIdx.x);
-  if (item_id >= a.n_items) return;
+  if (item_id >= item_count(a)) return;
   const ItemView v = item_view<C>(a, item_id, wave, l32);
   const SegInfo* segs = v.segs;
   const int32_t* rank_seg = v.rank_seg;
@@ -634,7 +648,7 @@ __global__ __launch_bounds__(256, 1) void attend_vrope_kernel(AttendArgs a) {
   const int64_t slot = v.slot, t_pos = v.t_pos;
   const uint16_t* qsrc = v.qsrc;
   const double* theta_rev = v.theta_rev;
-  const int64_t pidx = a.out_bf16 != nullptr ? slot : a.part_ptr[slot] + it.chunk;
+  const int64_t pidx = a.out_direct != nullptr ? slot : a.part_ptr[slot] + it.chunk;
   // this head-row's log2-sum-exp over the chunk (from the latent pass)
   const float lse2 = valid ? a.part_lse[pidx] * 1.4426950408889634f : 0.f;
 
@@ -808,8 +822,8 @@ __global__ __launch_bounds__(256, 1) void attend_vrope_kernel(AttendArgs a) {
   tile_barrier();
   close_segment(cs);
   if (!valid) return;
-  if (a.out_bf16 != nullptr) {
-    uint16_t* ob = a.out_bf16 + slot * a.dv + DC;
+  if (a.out_direct != nullptr && a.out_direct_bf16) {
+    uint16_t* ob = (uint16_t*)a.out_direct + slot * a.dv + DC;
 #pragma unroll
     for (int d = 0; d < 2; ++d)
 #pragma unroll
@@ -818,7 +832,7 @@ __global__ __launch_bounds__(256, 1) void attend_vrope_kernel(AttendArgs a) {
                                                           pack_bf16x2(rtot[d][4 * i + 2], rtot[d][4 * i + 3])};
     return;
   }
-  float* dst = a.part_o + pidx * a.dv + DC;
+  float* dst = (a.out_direct != nullptr ? (float*)a.out_direct : a.part_o) + pidx * a.dv + DC;
 #pragma unroll
   for (int d = 0; d < 2; ++d)
 #pragma unroll
@@ -831,70 +845,83 @@ __global__ __launch_bounds__(256, 1) void attend_vrope_kernel(AttendArgs a) {
 // ----------------------------------------------------------------------------
 // device half of the plan
 // ----------------------------------------------------------------------------
+// segment (storage order) holding storage row r: the last one whose kv_start <= r
+__device__ __forceinline__ int segment_of_row(const AttendArgs& a, int64_t r) {
+  int lo = 0, hi = a.n_segs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.segs[a.storage[mid]].kv_start <= r) lo = mid; else hi = mid - 1;
+  }
+  return a.storage[lo];
+}
+
 __global__ __launch_bounds__(256) void plan_slots_kernel(AttendArgs a) {
-  const unsigned char* ws = a.ws;
-  const SegInfo* segs = (const SegInfo*)(ws + a.hdr.off_segs);
-  const int32_t* rank_seg = (const int32_t*)(ws + a.hdr.off_rank);
-  const int32_t* storage = (const int32_t*)(ws + a.hdr.off_storage);
-  const ChunkInfo* chunks = (const ChunkInfo*)(ws + a.hdr.off_chunks);
-  const int32_t* prot_seg = (const int32_t*)(ws + a.hdr.off_prot_seg);
-  const int64_t* cum_local = (const int64_t*)(ws + a.hdr.off_cum_local);
+  const SegInfo* segs = a.segs;
+  const int64_t n_slots = a.dyn != nullptr ? a.dyn->n_slots : a.n_slots;
+  const int64_t n_parts = a.dyn != nullptr ? a.dyn->n_parts : a.n_parts;
   const int64_t nglob = a.n_rows * a.n_groups;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i <= a.n_slots;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i <= n_slots;
        i += (int64_t)gridDim.x * blockDim.x) {
-    if (i == a.n_slots) {
-      a.part_ptr[i] = a.hdr.n_parts;
+    if (i == n_slots) {
+      a.part_ptr[i] = n_parts;
       continue;
     }
     int s;
     int64_t base;
     if (i < nglob) {
       const int64_t r = i / a.n_groups, g = i - r * a.n_groups;
-      int lo = 0, hi = a.hdr.n_segs - 1;    // last segment (storage order) with kv_start <= r
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (segs[storage[mid]].kv_start <= r) lo = mid; else hi = mid - 1;
-      }
-      s = storage[lo];
+      s = segment_of_row(a, r);
       const SegInfo si = segs[s];
       base = si.cum_global + ((r - si.kv_start) * a.n_groups + g) * si.n_chunks;
     } else {
       const int64_t k = i - nglob;
       const int64_t ai = k / a.n_local, jj = k - ai * a.n_local;
-      s = prot_seg[ai];
-      base = a.hdr.global_parts + cum_local[ai] + jj * segs[s].n_chunks;
+      if (a.dyn == nullptr) {
+        s = a.prot_seg[ai];
+        base = a.global_parts + a.cum_local[ai] + jj * segs[s].n_chunks;
+      } else {
+        s = segment_of_row(a, a.prot[ai]);
+        const int64_t nch = segs[s].n_chunks;
+        base = a.global_parts + a.seg_local_base[s] + ((ai - a.seg_prot_lo[s]) * a.n_local + jj) * nch;
+      }
     }
     a.part_ptr[i] = base;
     if (a.part_seg != nullptr) {
       const SegInfo si = segs[s];
       for (int c = 0; c < si.n_chunks; ++c) {
-        const ChunkInfo ch = chunks[si.chunk_off + c];
-        a.part_seg[2 * (base + c)] = rank_seg[ch.first_rank];
-        a.part_seg[2 * (base + c) + 1] = rank_seg[ch.last_rank];
+        const ChunkInfo ch = a.chunks[si.chunk_off + c];
+        a.part_seg[2 * (base + c)] = a.rank_seg[ch.first_rank];
+        a.part_seg[2 * (base + c) + 1] = a.rank_seg[ch.last_rank];
       }
     }
   }
 }
 
 __global__ __launch_bounds__(256) void row_src_kernel(AttendArgs a) {
-  const int32_t* prot = (const int32_t*)(a.ws + a.hdr.off_prot);
+  const int32_t* prot = a.prot;
+  const int n_prot = a.dyn != nullptr ? a.dyn->n_prot : a.n_prot;
   for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < a.n_rows;
        r += (int64_t)gridDim.x * blockDim.x) {
-    int lo = 0, hi = a.n_prot;
+    int lo = 0, hi = n_prot;
     while (lo < hi) {
       const int mid = (lo + hi) >> 1;
       if (prot[mid] < r) lo = mid + 1; else hi = mid;
     }
-    a.row_src[r] = (lo < a.n_prot && prot[lo] == r) ? 1 : 0;
+    a.row_src[r] = (lo < n_prot && prot[lo] == r) ? 1 : 0;
   }
 }
 
+// part_ptr / part_seg (when part_ptr is set) and row_src (when set); grids cover
+// the host count of slots and rows (for a device plan, the capacity bound)
 hipError_t launch_plan(const AttendArgs& a, hipStream_t s) {
-  const int64_t n = a.n_slots + 1;
-  const unsigned blocks = (unsigned)std::min<int64_t>((n + 255) / 256, 8192);
-  plan_slots_kernel<<<dim3(blocks), dim3(256), 0, s>>>(a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.row_src == nullptr) return e;
+  if (a.part_ptr != nullptr) {
+    const int64_t n = a.n_slots + 1;
+    const unsigned blocks = (unsigned)std::min<int64_t>((n + 255) / 256, 8192);
+    plan_slots_kernel<<<dim3(blocks), dim3(256), 0, s>>>(a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (a.row_src == nullptr) return hipSuccess;
   const unsigned rb = (unsigned)std::min<int64_t>((a.n_rows + 255) / 256, 4096);
   row_src_kernel<<<dim3(rb), dim3(256), 0, s>>>(a);
   return hipGetLastError();

@@ -77,6 +77,28 @@ struct PlanHeader {
   int64_t total_bytes;
 };
 
+// Device-built plan (the protected set comes from device memory): the work
+// items of one (kind, segment, chunk) form a group; the groups are listed in a
+// launch order fixed on the host (largest upper-bound cost first), and the
+// device counts each group's items and lays them out in that order.
+struct ItemGroup {
+  int32_t kind;      // 0: Global head-rows of every row; 1: Local head-rows of protected rows
+  int32_t seg;
+  int32_t chunk;
+  int32_t n_items;   // kind 0: ceil(length * G / kTileRows); kind 1: counted on the device
+};
+
+// Counts of one device-planned call, written by the plan kernel before the
+// attention kernels read them.
+struct DynPlan {
+  int64_t n_slots;
+  int64_t n_parts;
+  int32_t n_items;
+  int32_t n_prot;
+  int32_t status;    // MLA_OK, or MLA_ERR_ROWS when the protected list was rejected
+  int32_t pad;
+};
+
 // ----------------------------------------------------------------------------
 // launchers (defined in the .hip files); all return hipError_t of the launch
 // ----------------------------------------------------------------------------
@@ -84,16 +106,32 @@ struct AttendArgs {
   const void* kv;
   const void* q_glob;
   const void* q_loc;
-  float* part_o;
-  float* part_lse;
-  int64_t* part_ptr;
-  int32_t* part_seg;
-  uint8_t* row_src;
-  const unsigned char* ws;   // device workspace holding the plan
+  float* part_o;             // [n_parts, dv] normalized partials (unused with out_direct)
+  float* part_lse;           // [n_parts] natural-log lse; with out_direct [slots] (may be NULL then,
+                             // except with a rotary value, whose second pass reads it)
+  int64_t* part_ptr;         // [n_slots + 1] CSR offsets of each slot's partials
+  int32_t* part_seg;         // [n_parts, 2] or NULL
+  uint8_t* row_src;          // [n_rows] or NULL
+  // plan tables in device memory
+  const SegInfo* segs;           // by segment index
+  const int32_t* rank_seg;       // segment index of each request-order rank
+  const int32_t* storage;        // segment indices by kv_start
+  const ChunkInfo* chunks;
+  const WorkItem* items;         // in launch order
+  const int32_t* prot;           // protected rows, ascending
+  const double* theta_rev;       // RoPE frequencies in revolutions
+  const int32_t* prot_seg;       // host plan: segment of each protected row
+  const int64_t* cum_local;      // host plan: Local partials before protected row a
+  const int32_t* seg_prot_lo;    // device plan: first protected-list index of each segment
+  const int64_t* seg_local_base; // device plan: Local partials before that segment's first protected row
+  const DynPlan* dyn;            // device plan: this call's counts (NULL: a host plan, counts below)
   int64_t n_rows;
   int64_t n_slots;
-  int32_t n_items;
+  int64_t n_parts;
+  int64_t global_parts;
+  int32_t n_items;           // host plan: work items; device plan: the bound the grid covers
   int32_t n_prot;
+  int32_t n_segs;
   int32_t n_groups;
   int32_t n_local;           // L_h = G*(hpg-1)
   int32_t d_latent;
@@ -101,17 +139,45 @@ struct AttendArgs {
   int32_t dv;                // head output width: d_latent, or d_latent + d_rope (rotary value)
   float scale_log2;          // softmax_scale * log2(e)
   int64_t local_slot_base;   // slot of Local head-row 0: n_rows * n_groups, or 0 without Global slots
-  uint16_t* out_bf16;        // if set: one chunk per slot, normalized O written here as bf16
-                             // [slots, dv] (part_o unused; part_lse [slots] if set)
-  PlanHeader hdr;            // copy of the plan header (offsets)
+  void* out_direct;          // if set: one chunk per slot, the normalized O written here [slots, dv]
+                             // (part_o unused)
+  int32_t out_direct_bf16;   // element type of out_direct: 1 bf16, 0 f32
 };
 
 hipError_t launch_plan(const AttendArgs& a, hipStream_t s);
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s);
 
+// n_slots_dev: if set, the device count of slots (n_slots is then the bound the grid covers)
 hipError_t launch_merge(int64_t n_slots, int32_t d_latent, const float* part_o,
                         const float* part_lse, const int64_t* part_ptr, int32_t out_dtype,
-                        void* out_o, float* out_lse, hipStream_t s);
+                        void* out_o, float* out_lse, hipStream_t s, const int64_t* n_slots_dev = nullptr);
+
+// device half of a device-built plan: protected-row ranges per segment, the
+// partial bases, the item counts and the work list (dplan.hip)
+struct DPlanArgs {
+  const SegInfo* segs;
+  const int32_t* storage;
+  const ItemGroup* groups;   // [n_item_groups] in launch order
+  const int32_t* prot;       // device protected rows
+  const int32_t* n_prot_dev; // device |A|
+  int32_t prot_cap;
+  int64_t n_rows;
+  int32_t n_segs;
+  int32_t n_item_groups;
+  int32_t n_groups;          // G
+  int32_t n_local;           // L_h
+  int64_t global_parts;
+  int64_t max_parts;         // the workspace's room for partials (chunked mode)
+  int32_t max_items;
+  DynPlan* dyn;
+  int32_t* seg_prot_lo;      // [n_segs]
+  int32_t* seg_prot_cnt;     // [n_segs]
+  int64_t* seg_local_base;   // [n_segs]
+  int32_t* group_base;       // [n_item_groups + 1]
+  WorkItem* items;           // [max_items]
+  int32_t* status_out;       // device int32 or NULL
+};
+hipError_t launch_dplan(const DPlanArgs& a, hipStream_t s);
 
 // ----------------------------------------------------------------------------
 // device helpers

@@ -14,8 +14,10 @@ __device__ __forceinline__ float wave_max(float v) {
 // One 64-lane wave per slot, 4 slots per 256-thread block.  Lane l owns the
 // float4 columns l, l+64, ... of the head-output row (d_c wide, or d_c + d_r
 // with a rotary value: the merge is linear, so both parts merge alike).
+// n_slots_dev, if set, holds the slot count (n_slots is then the bound of the grid).
 template <int DC, bool OUT_BF16>
-__global__ __launch_bounds__(256) void merge_kernel(int64_t n_slots, const float* __restrict__ part_o,
+__global__ __launch_bounds__(256) void merge_kernel(int64_t n_slots, const int64_t* __restrict__ n_slots_dev,
+                                                    const float* __restrict__ part_o,
                                                     const float* __restrict__ part_lse,
                                                     const int64_t* __restrict__ part_ptr,
                                                     void* __restrict__ out_o, float* __restrict__ out_lse) {
@@ -23,7 +25,7 @@ __global__ __launch_bounds__(256) void merge_kernel(int64_t n_slots, const float
   constexpr int PER = (NV + 63) / 64;         // float4 per lane
   const int lane = threadIdx.x & 63;
   const int64_t slot = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (slot >= n_slots) return;
+  if (slot >= (n_slots_dev != nullptr ? *n_slots_dev : n_slots)) return;
   const int64_t p0 = part_ptr[slot];
   const int n = (int)(part_ptr[slot + 1] - p0);
 
@@ -77,26 +79,22 @@ __global__ __launch_bounds__(256) void merge_kernel(int64_t n_slots, const float
 
 hipError_t launch_merge(int64_t n_slots, int32_t d_latent, const float* part_o, const float* part_lse,
                         const int64_t* part_ptr, int32_t out_dtype, void* out_o, float* out_lse,
-                        hipStream_t s) {
+                        hipStream_t s, const int64_t* n_slots_dev) {
   if (n_slots == 0) return hipSuccess;
   const dim3 grid((unsigned)((n_slots + 3) / 4)), block(256);
   const bool bf = out_dtype == MLA_BF16;
-  if (d_latent == 512) {
-    if (bf)
-      merge_kernel<512, true><<<grid, block, 0, s>>>(n_slots, part_o, part_lse, part_ptr, out_o, out_lse);
-    else
-      merge_kernel<512, false><<<grid, block, 0, s>>>(n_slots, part_o, part_lse, part_ptr, out_o, out_lse);
-  } else if (d_latent == 576) {   // rotary value: latent and RoPE dims
-    if (bf)
-      merge_kernel<576, true><<<grid, block, 0, s>>>(n_slots, part_o, part_lse, part_ptr, out_o, out_lse);
-    else
-      merge_kernel<576, false><<<grid, block, 0, s>>>(n_slots, part_o, part_lse, part_ptr, out_o, out_lse);
-  } else {
-    if (bf)
-      merge_kernel<64, true><<<grid, block, 0, s>>>(n_slots, part_o, part_lse, part_ptr, out_o, out_lse);
-    else
-      merge_kernel<64, false><<<grid, block, 0, s>>>(n_slots, part_o, part_lse, part_ptr, out_o, out_lse);
-  }
+#define MLA_MERGE(DC)                                                                                     \
+  (bf ? merge_kernel<DC, true><<<grid, block, 0, s>>>(n_slots, n_slots_dev, part_o, part_lse, part_ptr,  \
+                                                      out_o, out_lse)                                    \
+      : merge_kernel<DC, false><<<grid, block, 0, s>>>(n_slots, n_slots_dev, part_o, part_lse, part_ptr, \
+                                                       out_o, out_lse))
+  if (d_latent == 512)
+    MLA_MERGE(512);
+  else if (d_latent == 576)   // rotary value: latent and RoPE dims
+    MLA_MERGE(576);
+  else
+    MLA_MERGE(64);
+#undef MLA_MERGE
   return hipGetLastError();
 }
 

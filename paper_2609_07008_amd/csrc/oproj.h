@@ -19,7 +19,8 @@ struct OprojArgs {
   int32_t d_latent;
   int32_t d_model;
   int32_t n_pg;
-  int32_t z_bf16;            // 1: z is bf16 (Local pass only), 0: f32
+  int32_t z_bf16;            // 1: z is bf16, 0: f32
+  const int32_t* n_prot_dev; // if set: |A| in device memory, at most n_prot (the capacity the grid covers)
   int32_t glob_head[kMaxGroups];
 };
 

@@ -66,7 +66,14 @@ void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
   const int pg = bid / m_tiles;
   const int m0 = mt * OP_BM, n0 = nt * OP_BN;
 
-  const int64_t M = PASS == 0 ? (int64_t)a.n_prot : a.n_rows;
+  // protected rows in use: the host count, or the device count clamped to the capacity
+  int n_prot = a.n_prot;
+  if (a.n_prot_dev != nullptr) {
+    const int d = *a.n_prot_dev;
+    n_prot = d < 0 ? 0 : (d < a.n_prot ? d : a.n_prot);
+  }
+  const int64_t M = PASS == 0 ? (int64_t)n_prot : a.n_rows;
+  if (m0 >= M) return;   // a tile past the device count of protected rows
   const int heads_k = PASS == 0 ? gpp * (hpg - 1) : gpp;   // d_c-wide K blocks
   const int K = heads_k * DC;
   const uint16_t* A = (const uint16_t*)(PASS == 0 ? a.o_loc : a.o_glob);
@@ -84,12 +91,12 @@ void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
         flag = 1;
       } else {
         orow = (int)m;
-        int lo = 0, hi = a.n_prot;          // binary search in the sorted protected rows
+        int lo = 0, hi = n_prot;            // binary search in the sorted protected rows
         while (lo < hi) {
           const int mid = (lo + hi) >> 1;
           if (a.prot_rows[mid] < (int)m) lo = mid + 1; else hi = mid;
         }
-        flag = (lo < a.n_prot && a.prot_rows[lo] == (int)m) ? 1 : 0;
+        flag = (lo < n_prot && a.prot_rows[lo] == (int)m) ? 1 : 0;
       }
     }
     row_flag[i] = flag;
@@ -213,21 +220,25 @@ void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
         if (n >= cw) continue;                                     // cw is a multiple of 32
         const int64_t off = orow * a.d_model + (int64_t)pg * cw + n;
         f32x4 v = {acc[mi][ni][4 * i], acc[mi][ni][4 * i + 1], acc[mi][ni][4 * i + 2], acc[mi][ni][4 * i + 3]};
-        if (PASS == 0 && a.z_bf16) {   // the artifact of the offline producer
-          *(u32x2*)((uint16_t*)a.z + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-          continue;
-        }
-        float* dst = a.z + off;
         if (PASS == 1) {
           if (flag) {
-            if (hpg > 1) v += *(const f32x4*)dst;   // the Local pass wrote this row first
+            if (hpg > 1) {   // the Local pass wrote this row first
+              if (a.z_bf16) {
+                const u32x2 zl = *(const u32x2*)((const uint16_t*)a.z + off);
+                v += f32x4{bf16_lo(zl[0]), bf16_hi(zl[0]), bf16_lo(zl[1]), bf16_hi(zl[1])};
+              } else {
+                v += *(const f32x4*)(a.z + off);
+              }
+            }
           } else {
             const u32x2 zz = *(const u32x2*)(zoff + off);
-            v += f32x4{__uint_as_float(zz[0] << 16), __uint_as_float(zz[0] & 0xFFFF0000u),
-                       __uint_as_float(zz[1] << 16), __uint_as_float(zz[1] & 0xFFFF0000u)};
+            v += f32x4{bf16_lo(zz[0]), bf16_hi(zz[0]), bf16_lo(zz[1]), bf16_hi(zz[1])};
           }
         }
-        *(f32x4*)dst = v;
+        if (a.z_bf16)
+          *(u32x2*)((uint16_t*)a.z + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        else
+          *(f32x4*)(a.z + off) = v;
       }
   }
 }

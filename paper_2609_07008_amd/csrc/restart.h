@@ -16,7 +16,11 @@
 //     the loop ends even when a raise cannot help (an infinite score, or a
 //     reference so large that adding 128 does not change it).  Weights that
 //     still overflow then give inf / inf = NaN in that head-row's output, as
-//     IEEE arithmetic does.
+//     IEEE arithmetic does.  Each pass ends at the first tile where some
+//     head-row votes, so finite inputs reach the cap only when an item's
+//     head-rows need raises at more than 15 distinct tiles; a head-row left
+//     below its ideal reference is still exact while its weights stay below
+//     the fp32 range (2^128).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -27,7 +31,7 @@ namespace mla {
 
 constexpr float kRestartSum = 0x1p64f;    // a lane's tile weight sum at or above this votes
 constexpr float kOverflowRaise = 128.f;   // raise (log2 units) after an fp32 overflow
-constexpr int kMaxAttempts = 8;           // passes over one work item: at most 7 restarts
+constexpr int kMaxAttempts = 16;          // passes over one work item: at most 15 restarts
 
 // does this lane's tile weight sum ask for a higher reference?
 __host__ __device__ inline bool restart_vote(float rsum) { return rsum >= kRestartSum; }

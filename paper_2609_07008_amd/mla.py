@@ -20,6 +20,7 @@ MLA_BF16, MLA_F32 = 0, 1
 STATUS = {0: "MLA_OK", 1: "MLA_ERR_NULL", 2: "MLA_ERR_SHAPE", 3: "MLA_ERR_UNSUPPORTED",
           4: "MLA_ERR_SEGMENTS", 5: "MLA_ERR_ROWS", 6: "MLA_ERR_WORKSPACE", 7: "MLA_ERR_HIP"}
 EXPORTS = ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
+           "mla_online_plan_query", "mla_online_plan", "mla_online_attend_planned", "mla_sliced_oproj_add_planned",
            "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query", "mla_protected_rows",
            "mla_moe_fanout", "mla_shared_wb", "mla_status_str", "mla_last_error_detail", "mla_version")
 
@@ -41,6 +42,15 @@ class Segment(ctypes.Structure):
     _fields_ = [("kv_start", ctypes.c_int64), ("length", ctypes.c_int64), ("req_offset", ctypes.c_int64)]
 
 
+class PlanInfo(ctypes.Structure):
+    """mla_plan_info: host description of a plan built by mla_online_plan."""
+    _fields_ = [("geom", Geom), ("n_rows", ctypes.c_int64), ("split_keys", ctypes.c_int64),
+                ("max_slots", ctypes.c_int64), ("max_parts", ctypes.c_int64), ("n_segs", ctypes.c_int32),
+                ("prot_cap", ctypes.c_int32), ("max_items", ctypes.c_int32), ("one_chunk", ctypes.c_int32),
+                ("plan_bytes", ctypes.c_size_t), ("ws_bytes", ctypes.c_size_t), ("layout", ctypes.c_int64 * 24),
+                ("check", ctypes.c_uint64)]
+
+
 class ProtectCfg(ctypes.Structure):
     _fields_ = [("query_seg", ctypes.c_int32), ("edge_rows", ctypes.c_int32), ("tail_rows", ctypes.c_int64),
                 ("budget", ctypes.c_double)]
@@ -57,6 +67,11 @@ def _load(path: str = LIB_PATH):
     lib.mla_online_attend.argtypes = [GP, SP, I32, P, I32, I64, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.mla_segment_merge.argtypes = [I64, I32, P, P, P, I32, P, P, P]
     lib.mla_sliced_oproj_add.argtypes = [GP, I64, P, P, P, P, I32, P, P, P, P]
+    IP = ctypes.POINTER(PlanInfo)
+    lib.mla_online_plan_query.argtypes = [GP, SP, I32, I64, I32, IP]
+    lib.mla_online_plan.argtypes = [GP, SP, I32, I64, I32, IP, P, SZ, P]
+    lib.mla_online_attend_planned.argtypes = [GP, IP, P, P, P, P, P, P, I32, P, P, P, P, P, P, P, SZ, P]
+    lib.mla_sliced_oproj_add_planned.argtypes = [GP, IP, P, P, P, P, P, P, P, I32, P, P]
     lib.mla_offline_produce_query.argtypes = [GP, SP, I32, ctypes.POINTER(SZ)]
     lib.mla_offline_produce.argtypes = [GP, SP, I32, P, P, P, P, I32, P, P, SZ, P]
     lib.mla_protected_rows_query.argtypes = [SP, I32, ctypes.POINTER(SZ)]
@@ -64,7 +79,8 @@ def _load(path: str = LIB_PATH):
     lib.mla_moe_fanout.argtypes = [I64, I32, P, I32, I32, ctypes.c_float, P, P, P, P, P]
     lib.mla_shared_wb.argtypes = [I64, I32, I32, P, P, I32, P, P]
     for f in ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
-              "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query",
+              "mla_online_plan_query", "mla_online_plan", "mla_online_attend_planned",
+              "mla_sliced_oproj_add_planned", "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query",
               "mla_protected_rows", "mla_moe_fanout", "mla_shared_wb"):
         getattr(lib, f).restype = ctypes.c_int
     lib.mla_status_str.argtypes = [ctypes.c_int]
@@ -155,6 +171,50 @@ def sliced_oproj_add(geom, n_rows, o_glob, o_loc, glob_head, prot_rows_d, n_prot
     _check(LIB.mla_sliced_oproj_add(ctypes.byref(g), int(n_rows), _ptr(o_glob), _ptr(o_loc), _ptr(gh),
                                     _ptr(prot_rows_d), int(n_prot), _ptr(w_o), _ptr(z_off), _ptr(z),
                                     _stream(stream)))
+
+
+def plan_query(geom, segs, split_keys: int, prot_cap: int) -> PlanInfo:
+    """Host-only: the PlanInfo (sizes and bounds) of a plan."""
+    g = make_geom(geom)
+    sarr, ns = make_segments(segs)
+    info = PlanInfo()
+    _check(LIB.mla_online_plan_query(ctypes.byref(g), sarr, ns, int(split_keys), int(prot_cap), ctypes.byref(info)))
+    return info
+
+
+def online_plan(geom, segs, split_keys: int, prot_cap: int, plan, stream=None) -> PlanInfo:
+    """mla_online_plan: writes the plan image into the device tensor `plan` and
+    returns its PlanInfo."""
+    g = make_geom(geom)
+    sarr, ns = make_segments(segs)
+    info = PlanInfo()
+    _check(LIB.mla_online_plan(ctypes.byref(g), sarr, ns, int(split_keys), int(prot_cap), ctypes.byref(info),
+                               _ptr(plan), plan.numel() * plan.element_size(), _stream(stream)))
+    return info
+
+
+def online_attend_planned(geom, info, plan, prot_rows, n_prot, kv, q_glob, q_loc, out_o, out_lse=None,
+                          part_ptr=None, part_seg=None, row_src=None, status=None, workspace=None, stream=None):
+    """mla_online_attend_planned: every argument a device tensor (prot_rows int32,
+    n_prot int32 [1]); out_o bfloat16 or float32 [info.max_slots, d_v]."""
+    g = make_geom(geom)
+    out = MLA_BF16 if out_o.dtype == torch.bfloat16 else MLA_F32
+    _check(LIB.mla_online_attend_planned(ctypes.byref(g), ctypes.byref(info), _ptr(plan), _ptr(prot_rows),
+                                         _ptr(n_prot), _ptr(kv), _ptr(q_glob), _ptr(q_loc), out, _ptr(out_o),
+                                         _ptr(out_lse), _ptr(part_ptr), _ptr(part_seg), _ptr(row_src), _ptr(status),
+                                         _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                         _stream(stream)))
+
+
+def sliced_oproj_add_planned(geom, info, o_glob, o_loc, glob_head, prot_rows, n_prot, w_o, z_off, z, stream=None):
+    """mla_sliced_oproj_add_planned: |A| from the device tensor n_prot; z float32
+    or bfloat16."""
+    g = make_geom(geom)
+    gh = np.ascontiguousarray(glob_head, dtype=np.int32)
+    zt = MLA_BF16 if z.dtype == torch.bfloat16 else MLA_F32
+    _check(LIB.mla_sliced_oproj_add_planned(ctypes.byref(g), ctypes.byref(info), _ptr(o_glob), _ptr(o_loc), _ptr(gh),
+                                            _ptr(prot_rows), _ptr(n_prot), _ptr(w_o), _ptr(z_off), zt, _ptr(z),
+                                            _stream(stream)))
 
 
 def offline_produce_query(geom, segs) -> int:

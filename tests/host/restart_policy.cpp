@@ -56,7 +56,7 @@ int main() {
   CHECK(restart_raise(1.f) == -INFINITY);
   CHECK(restart_raise(std::nextafterf(two64, 0.f)) == -INFINITY);
   // attempts
-  CHECK(kMaxAttempts == 8);
+  CHECK(kMaxAttempts == 16);
   for (int a = 0; a + 1 < kMaxAttempts; ++a) CHECK(restart_allowed(a));
   CHECK(!restart_allowed(kMaxAttempts - 1));
   CHECK(!restart_allowed(kMaxAttempts));
@@ -74,7 +74,8 @@ int main() {
   CHECK(passes(0.f, 63.9f) == 1);
   CHECK(passes(0.f, 100.f) == 2);         // raised by log2(2^100): exact
   CHECK(passes(0.f, 288.5f) == 3);        // +200 nats: overflow (+128), then finite
-  CHECK(passes(0.f, 1000.f) == kMaxAttempts);   // more than 7 raises of 128 would be needed
+  CHECK(passes(0.f, 1000.f) == 9);        // seven overflow raises of 128, one of log2(2^104), done
+  CHECK(passes(0.f, 3000.f) == kMaxAttempts);   // more than 15 raises of 128 would be needed
   CHECK(passes(0.f, INFINITY) == kMaxAttempts); // an infinite score: bounded, then NaN
   CHECK(passes(1e38f, 1e38f * 2.f) == kMaxAttempts);   // raises lost to rounding: bounded
   CHECK(passes(NAN, 5.f) == 1);           // a NaN reference: NaN weights, no vote

@@ -294,3 +294,97 @@ def test_value_rope_geometry_checks():
     ws = ctypes.c_size_t()
     sarr, ns = mla.make_segments(segs)
     assert mla.LIB.mla_offline_produce_query(ctypes.byref(g), sarr, ns, ctypes.byref(ws)) == 2
+
+
+# ----------------------------------------------------------------------------
+# plan-once path: sizes and bounds on the host, and the checks made before any
+# device work (no GPU call is reached by these cases)
+# ----------------------------------------------------------------------------
+def _local_items(wl, split, prot):
+    """Work items the device plan lays out for the Local heads of protected set
+    `prot`: per segment and chunk, ceil(|A in segment| * L_h / 128)."""
+    g = wl.geom
+    lh = g.n_groups * (g.heads_per_group - 1)
+    if lh == 0:
+        return 0
+    chunks = M.segment_chunks(wl.segs, split)
+    seg, _, _ = M.row_geometry(wl.segs)
+    cnt = np.bincount(seg[np.asarray(prot, dtype=np.int64)], minlength=len(wl.segs))
+    return sum(len(chunks[s]) * -(-int(cnt[s]) * lh // 128) for s in range(len(wl.segs)))
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 5])
+@pytest.mark.parametrize("split", [0, 4096, 10 ** 9])
+def test_plan_bounds_cover_every_protected_set(mla, cfg, split):
+    wl = make_workload(cfg)
+    g = wl.geom
+    if cfg == 5 and split == 0:
+        pytest.skip("70M per-segment partials at 256K: covered by the closed form of the size query")
+    split = min(split, wl.n_rows)
+    rng = np.random.default_rng(cfg)
+    lh = g.n_groups * (g.heads_per_group - 1)
+    for cap in sorted({wl.n_prot, wl.n_rows, max(1, wl.n_prot // 3)}):
+        info = mla.plan_query(g, wl.segs, split, cap)
+        assert info.max_slots == wl.n_rows * g.n_groups + cap * lh
+        assert info.prot_cap == cap and info.n_rows == wl.n_rows and info.split_keys == split
+        assert info.plan_bytes % 256 == 0 and info.ws_bytes % 256 == 0
+        assert info.one_chunk == int(split >= wl.n_rows or len(wl.segs) == 1)
+        glob_items = sum(len(c) * -(-int(ln) * g.n_groups // 128)
+                         for c, (_, ln, _) in zip(M.segment_chunks(wl.segs, split), wl.segs))
+        # protected sets of `cap` rows: the workload's own (when it fits), the rows
+        # of the segments with the most chunks, and random ones
+        sets = [np.sort(rng.choice(wl.n_rows, size=cap, replace=False)) for _ in range(3)]
+        if wl.n_prot <= cap:
+            sets.append(np.asarray(wl.prot_rows))
+        seg, _, _ = M.row_geometry(wl.segs)
+        nch = np.array([len(c) for c in M.segment_chunks(wl.segs, split)])
+        sets.append(np.sort(np.argsort(-nch[seg], kind="stable")[:cap]))
+        for prot in sets:
+            assert glob_items + _local_items(wl, split, prot) <= info.max_items
+            if cfg <= 3:
+                _, ptr, _ = M.enumerate_plan(wl.segs, g.n_groups, g.heads_per_group, prot, split)
+                assert int(ptr[-1]) <= info.max_parts
+
+
+def test_plan_query_rejects(mla):
+    wl = _tiny()
+    for cap in (-1, wl.n_rows + 1):
+        with pytest.raises(mla.MlaError) as e:
+            mla.plan_query(wl.geom, wl.segs, 0, cap)
+        assert e.value.status == 2
+    with pytest.raises(mla.MlaError) as e:
+        mla.plan_query(_geom(wl, d_latent=128, d_rope=32), wl.segs, 0, 1)
+    assert e.value.status == 3
+    segs = wl.segs.copy()
+    segs[1, 0] += 1
+    with pytest.raises(mla.MlaError) as e:
+        mla.plan_query(wl.geom, segs, 0, 1)
+    assert e.value.status == 4
+
+
+def test_planned_calls_check_the_plan_first(mla):
+    """A changed plan description or another geometry is refused on the host,
+    before any pointer is used (the device pointers here are all NULL)."""
+    import ctypes
+    wl = _tiny()
+    info = mla.plan_query(wl.geom, wl.segs, 0, wl.n_prot)
+    g = mla.make_geom(wl.geom)
+
+    def attend(gm, inf):
+        return mla.LIB.mla_online_attend_planned(ctypes.byref(gm), ctypes.byref(inf), None, None, None, None, None,
+                                                 None, 0, None, None, None, None, None, None, None, 0, None)
+
+    def oproj(gm, inf):
+        gh = np.zeros(wl.geom.n_groups, dtype=np.int32)
+        return mla.LIB.mla_sliced_oproj_add_planned(ctypes.byref(gm), ctypes.byref(inf), None, None,
+                                                    gh.ctypes.data_as(ctypes.c_void_p), None, None, None, None, 1,
+                                                    None, None)
+
+    assert attend(g, info) == 1 and oproj(g, info) == 1          # intact: fails later, on a NULL pointer
+    bad = mla.PlanInfo.from_buffer_copy(info)
+    bad.max_items += 1
+    assert attend(g, bad) == 2 and oproj(g, bad) == 2
+    assert "mla_online_plan" in mla.LIB.mla_last_error_detail().decode()
+    other = mla.make_geom(_geom(wl, softmax_scale=0.5))
+    assert attend(other, info) == 2 and oproj(other, info) == 2
+    assert "geometry" in mla.LIB.mla_last_error_detail().decode()

@@ -1,0 +1,312 @@
+"""The plan-once path with the protected set in device memory
+(mla_online_plan, mla_online_attend_planned, mla_sliced_oproj_add_planned).
+
+* Against the host-plan path (mla_online_attend + mla_segment_merge +
+  mla_sliced_oproj_add) on the same inputs: merged head outputs, lse, z and the
+  bookkeeping are bit-identical (each head-row's arithmetic does not depend on
+  which work item carries it: tiles past a head-row's visible keys add exact
+  zeros, and a restart leaves non-voting head-rows unchanged).
+* Against the fp64 oracle at full size, in the benchmark's launch.
+* Chained on the device (Alg. 2: ProtectedRows, then SelectiveMLA, the sliced
+  projection and W_b z): mla_protected_rows -> attend -> o-proj (bf16 z) ->
+  mla_shared_wb with no host copy of the protected rows, against the oracle's
+  protected set, step and second projection.
+* Device validation: a rejected protected list writes status MLA_ERR_ROWS and
+  no output row.
+* Graph capture: attend + o-proj captured once and replayed, also after the
+  protected set in the same device buffers changes.
+"""
+import numpy as np
+import pytest
+
+from oracle import mla_oracle as M
+from workloads import make_custom, make_workload, round_bf16, wb_inputs
+
+from parity import check, check_bookkeeping, compare_rows, run, segment_edge_sample
+
+pytestmark = pytest.mark.gpu
+
+CUSTOM = {
+    "ragged": dict(doc_lens=[1, 2, 63, 64, 65, 130, 7], req_perm=[4, 0, 6, 2, 5, 1, 3], tq=37, H=16, G=2,
+                   d_model=256, prot_frac=0.1),
+    "dense_proj": dict(doc_lens=[70, 33, 128], req_perm=[2, 0, 1], tq=20, H=16, G=2, d_model=256, n_pg=1,
+                       prot_frac=0.15),
+    "wide_groups": dict(doc_lens=[96, 40], req_perm=[1, 0], tq=9, H=32, G=4, d_model=512, prot_frac=0.2),
+    "single_segment": dict(doc_lens=[200], req_perm=None, tq=0, H=8, G=1, d_model=128, prot_frac=0.3),
+    "no_local_heads": dict(doc_lens=[65, 3, 64], req_perm=[1, 2, 0], tq=5, H=4, G=4, d_model=128, prot_frac=0.2),
+}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    from paper_2609_07008_amd import mla  # noqa: F401
+    yield
+
+
+def _bits(t):
+    import torch
+    size = t.element_size()
+    if size == 1:
+        return t.contiguous().clone()
+    return t.contiguous().view({2: torch.int16, 4: torch.int32, 8: torch.int64}[size]).clone()
+
+
+def _device_prot(wl, cap):
+    """prot_rows padded to the capacity (the padding must never be read) and |A|, on the device."""
+    import torch
+    p = np.full(max(cap, 1), -7, dtype=np.int32)
+    p[: wl.n_prot] = np.asarray(wl.prot_rows, dtype=np.int32)
+    return torch.from_numpy(p).cuda(), torch.tensor([wl.n_prot], dtype=torch.int32, device="cuda")
+
+
+def _q_loc_padded(inputs, wl, cap):
+    """q_loc with room for `cap` protected rows (rows past |A| left NaN: never read)."""
+    import torch
+    g = wl.geom
+    hl = g.heads_per_group - 1
+    if hl == 0:
+        return None
+    q = torch.full((max(cap, 1), g.n_groups, hl, g.d_latent + g.d_rope), float("nan"), dtype=torch.bfloat16,
+                   device="cuda")
+    if wl.n_prot:
+        q[: wl.n_prot] = inputs["q_loc"]
+    return q
+
+
+def _planned(wl, split, cap, inputs, z_dtype=None, out_dtype=None):
+    import torch
+    from paper_2609_07008_amd import mla, step
+    st = step.PlannedStep(wl.geom, wl.segs, wl.glob_head, split, cap,
+                          out_dtype=mla.MLA_BF16 if out_dtype is None else out_dtype,
+                          z_dtype=torch.float32 if z_dtype is None else z_dtype)
+    st.out_o.view(torch.uint8).fill_(0xFF)
+    prot_d, n_d = _device_prot(wl, cap)
+    st.run(prot_d, n_d, inputs["kv"], inputs["q_glob"], _q_loc_padded(inputs, wl, cap), inputs["w_o"],
+           inputs["z_off"])
+    torch.cuda.synchronize()
+    assert int(st.status.item()) == 0
+    return st
+
+
+@pytest.mark.parametrize("name", sorted(CUSTOM))
+@pytest.mark.parametrize("split", [0, 100, 10 ** 9])
+@pytest.mark.parametrize("cap", ["exact", "all_rows"])
+def test_planned_equals_host_path(name, split, cap):
+    wl = make_custom(d_c=512, d_r=64, seed=300 + sorted(CUSTOM).index(name), fp32=False, **CUSTOM[name])
+    split = min(split, wl.n_rows)
+    host, inputs = run(wl, split)
+    c = wl.n_prot if cap == "exact" else wl.n_rows
+    st = _planned(wl, split, c, inputs)
+    n_slots, n_parts = host.n_slots, host.n_parts
+    assert torch_equal(st.out_o[:n_slots], host.out_o)
+    assert torch_equal(st.out_lse[:n_slots], host.out_lse)
+    assert torch_equal(st.part_ptr[: n_slots + 1], host.part_ptr)
+    assert torch_equal(st.part_seg[:n_parts], host.part_seg)
+    assert torch_equal(st.row_src, host.row_src)
+    assert torch_equal(st.z, host.z)
+    assert torch_equal(st.out_o[n_slots:], None)     # rows past the slots of |A| stay untouched
+
+
+def torch_equal(a, b):
+    import torch
+    if b is None:                                     # never written: still the 0xFF fill
+        return bool(torch.all(a.contiguous().view(torch.uint8) == 0xFF))
+    return torch.equal(_bits(a), _bits(b))
+
+
+def test_planned_tiny_and_f32_output():
+    """The tiny exactness workload (64 + 16 latent): bf16 head outputs against the
+    oracle through the whole step; f32 head outputs (attention and merge only,
+    the o-proj takes bf16) bit-identical to the host path's f32 merge output."""
+    import torch
+    from paper_2609_07008_amd import device_inputs, mla, step
+    from parity import artifact_bf16
+    wl = make_workload(1)
+    z_off = artifact_bf16(wl)
+    inputs = device_inputs.upload(wl, z_off=z_off)
+    for split in (0, 10 ** 9):
+        split = min(split, wl.n_rows)
+        st = _planned(wl, split, wl.n_rows, inputs)
+        check_bookkeeping(wl, st, split)
+        compare_rows(wl, st, np.arange(wl.n_rows), z_off)
+        host = step.OnlineStep(wl.geom, wl.segs, wl.prot_rows, wl.glob_head, split, out_dtype=mla.MLA_F32)
+        host.attend(inputs["kv"], inputs["q_glob"], inputs["q_loc"])
+        host.merge()
+        pl = step.PlannedStep(wl.geom, wl.segs, wl.glob_head, split, wl.n_rows, out_dtype=mla.MLA_F32)
+        prot_d, n_d = _device_prot(wl, wl.n_rows)
+        pl.attend(prot_d, n_d, inputs["kv"], inputs["q_glob"], _q_loc_padded(inputs, wl, wl.n_rows))
+        torch.cuda.synchronize()
+        assert torch_equal(pl.out_o[: host.n_slots], host.out_o)
+        assert torch_equal(pl.out_lse[: host.n_slots], host.out_lse)
+        with pytest.raises(ValueError):
+            pl.oproj(prot_d, n_d, inputs["w_o"], inputs["z_off"])
+
+
+@pytest.mark.parametrize("cfg,split,cap", [(2, 0, "exact"), (2, 10 ** 9, "all_rows"), (3, 8192, "exact"),
+                                           (5, 10 ** 9, "exact_plus")])
+def test_planned_full_workload(cfg, split, cap):
+    from paper_2609_07008_amd import device_inputs
+    wl = make_workload(cfg)
+    split = min(split, wl.n_rows) if split else 0
+    inputs = device_inputs.upload(wl)
+    c = {"exact": wl.n_prot, "all_rows": wl.n_rows, "exact_plus": wl.n_prot + 4096}[cap]
+    st = _planned(wl, split, c, inputs)
+    check_bookkeeping(wl, st, split, full_part_seg=(cfg <= 3))
+    g = wl.geom
+    kv = wl.kv()
+    keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    compare_rows(wl, st, segment_edge_sample(wl, seed=cfg), None, kv=kv, keys=keys)
+
+
+def test_chained_protected_set_step_and_wb():
+    """ProtectedRows -> SelectiveMLA -> merge -> sliced o-proj + RestoreAndReplace
+    -> W_b z on the device, the protected rows and |A| never copied to the host
+    before the step has been enqueued (they are read back afterwards to check)."""
+    import torch
+    from paper_2609_07008_amd import device_inputs, mla, step
+    kw = dict(doc_lens=[400, 700, 257, 520], req_perm=[2, 0, 3, 1], tq=40, H=16, G=2, d_c=512, d_r=64,
+              d_model=256, fp32=False, seed=61)
+    base = make_custom(prot_rows=np.zeros(0, dtype=np.int32), **kw)
+    segs, n = base.segs, base.n_rows
+    qseg = len(kw["doc_lens"])
+    rng = np.random.default_rng(62)
+    flags = np.zeros(n, dtype=np.uint8)
+    flags[rng.choice(n, size=n // 50, replace=False)] |= 2
+    flags[rng.choice(n, size=n // 100, replace=False)] |= 1
+    scores = rng.standard_normal(n).astype(np.float32)
+    scores[rng.choice(n, size=64, replace=False)] = 0.5          # ties
+    edge, tail, budget = 16, 256, 0.2
+    a_ref = M.protected_rows(segs, qseg, flags, scores, edge, tail, budget)
+    wl = make_custom(prot_rows=a_ref, **kw)
+    assert np.array_equal(wl.segs, segs)
+    inputs = device_inputs.upload(wl)
+    w_b_in = wb_inputs(n, wl.geom.d_model, 192, seed=63)[1]
+    w_b = device_inputs.to_bf16(w_b_in)
+
+    prot_d = torch.empty((n,), dtype=torch.int32, device="cuda")
+    n_d = torch.empty((1,), dtype=torch.int32, device="cuda")
+    ws_p = torch.empty(mla.protected_rows_query(segs), dtype=torch.uint8, device="cuda")
+    st = step.PlannedStep(wl.geom, segs, wl.glob_head, n, n, z_dtype=torch.bfloat16)
+    q_loc = _q_loc_padded(inputs, wl, n)
+    y = torch.empty((n, 192), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    mla.protected_rows(segs, qseg, edge, tail, budget, torch.from_numpy(flags).cuda(),
+                       torch.from_numpy(scores).cuda(), prot_d, n_d, ws_p)
+    st.run(prot_d, n_d, inputs["kv"], inputs["q_glob"], q_loc, inputs["w_o"], inputs["z_off"])
+    mla.shared_wb(st.z, w_b, y)
+    torch.cuda.synchronize()
+
+    assert int(st.status.item()) == 0
+    assert int(n_d.item()) == len(a_ref)
+    assert np.array_equal(prot_d[: len(a_ref)].cpu().numpy(), a_ref)
+    check_bookkeeping(wl, st, n)
+    ref = compare_rows(wl, st, np.arange(n), wl.z_off())
+    # W_b on the step's own bf16 z (the kernel's bound), and against the oracle's z
+    z_gpu = st.z.float().cpu().numpy().astype(np.float64)
+    y_gpu = y.cpu().numpy().astype(np.float64)
+    w64 = w_b_in.astype(np.float64)
+    y_own = M.shared_wb(z_gpu, w64)
+    bound = 3e-4 * (np.abs(z_gpu) @ np.abs(w64).T) + 1e-7
+    assert np.all(np.abs(y_gpu - y_own) <= bound)
+    check("y = W_b z", y_gpu, M.shared_wb(ref.z, w64))
+
+
+@pytest.mark.parametrize("case", ["over_capacity", "negative_count", "unsorted", "duplicate", "row_past_end",
+                                  "negative_row"])
+def test_device_list_rejected(case):
+    import torch
+    from paper_2609_07008_amd import device_inputs, step
+    wl = make_custom([70, 90, 66], req_perm=[2, 0, 1], tq=12, H=16, G=2, d_c=512, d_r=64, d_model=256,
+                     fp32=False, seed=71, prot_frac=0.2)
+    inputs = device_inputs.upload(wl)
+    cap = wl.n_prot + 3
+    p = np.full(cap, 0, dtype=np.int32)
+    p[: wl.n_prot] = wl.prot_rows
+    n_prot = wl.n_prot
+    if case == "over_capacity":
+        n_prot = cap + 1
+    elif case == "negative_count":
+        n_prot = -1
+    elif case == "unsorted":
+        p[[3, 4]] = p[[4, 3]]
+    elif case == "duplicate":
+        p[5] = p[4]
+    elif case == "row_past_end":
+        p[wl.n_prot - 1] = wl.n_rows
+    else:
+        p[0] = -1
+    st = step.PlannedStep(wl.geom, wl.segs, wl.glob_head, wl.n_rows, cap)
+    st.out_o.view(torch.uint8).fill_(0xFF)
+    st.out_lse.view(torch.uint8).fill_(0xFF)
+    q_loc = _q_loc_padded(inputs, wl, cap)
+    st.attend(torch.from_numpy(p).cuda(), torch.tensor([n_prot], dtype=torch.int32, device="cuda"),
+              inputs["kv"], inputs["q_glob"], q_loc)
+    torch.cuda.synchronize()
+    assert int(st.status.item()) == 5                        # MLA_ERR_ROWS
+    assert torch_equal(st.out_o, None) and torch_equal(st.out_lse, None)
+    # the same plan and workspace then serve a valid list
+    prot_d, n_d = _device_prot(wl, cap)
+    st.attend(prot_d, n_d, inputs["kv"], inputs["q_glob"], q_loc)
+    torch.cuda.synchronize()
+    assert int(st.status.item()) == 0
+    host, _ = run(wl, wl.n_rows, inputs=inputs)
+    assert torch_equal(st.out_o[: host.n_slots], host.out_o)
+
+
+def test_planned_graph_replay_follows_device_set():
+    """attend + o-proj captured once; each replay reads the protected set that
+    the device buffers hold at that time, so a new set (another layer's) needs
+    no new capture.  Every replay equals the eager call on the same set."""
+    import torch
+    from paper_2609_07008_amd import device_inputs, step
+    kw = dict(doc_lens=[70, 90, 66], req_perm=[2, 0, 1], tq=12, H=16, G=2, d_c=512, d_r=64, d_model=256,
+              fp32=False, seed=73)
+    wl_a = make_custom(prot_frac=0.2, **kw)
+    rng = np.random.default_rng(74)
+    n = wl_a.n_rows
+    b_rows = np.unique(np.concatenate([rng.choice(n - 12, size=40, replace=False), np.arange(n - 12, n)]))
+    wl_b = make_custom(prot_rows=b_rows, glob_head=wl_a.glob_head, **kw)
+    assert wl_a.n_prot != wl_b.n_prot
+    cap = n
+    ins_a, ins_b = device_inputs.upload(wl_a), device_inputs.upload(wl_b)
+    q_a, q_b = _q_loc_padded(ins_a, wl_a, cap), _q_loc_padded(ins_b, wl_b, cap)
+    eager = {}
+    for key, wl, ins, q in (("a", wl_a, ins_a, q_a), ("b", wl_b, ins_b, q_b)):
+        e = step.PlannedStep(wl.geom, wl.segs, wl.glob_head, n, cap)
+        pd, nd = _device_prot(wl, cap)
+        e.run(pd, nd, ins["kv"], ins["q_glob"], q, ins["w_o"], ins["z_off"])
+        torch.cuda.synchronize()
+        ns = n * wl.geom.n_groups + wl.n_prot * wl.geom.n_local      # rows of out_o this set writes
+        eager[key] = (_bits(e.out_o[:ns]), _bits(e.out_lse[:ns]), _bits(e.z), ns)
+    # one step object, one set of device buffers for the protected set and q_loc
+    st = step.PlannedStep(wl_a.geom, wl_a.segs, wl_a.glob_head, n, cap)
+    prot_d, n_d = _device_prot(wl_a, cap)
+    q_d = q_a.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            st.run(prot_d, n_d, ins_a["kv"], ins_a["q_glob"], q_d, ins_a["w_o"], ins_a["z_off"], stream=side)
+    torch.cuda.synchronize()
+    for rep, key in enumerate(["a", "b", "a", "b"]):
+        wl, q = (wl_a, q_a) if key == "a" else (wl_b, q_b)
+        pd, nd = _device_prot(wl, cap)
+        prot_d.copy_(pd)
+        n_d.copy_(nd)
+        q_d.copy_(q)
+        for t in (st.out_o, st.out_lse, st.z):
+            t.view(torch.uint8).fill_(0xFF)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert int(st.status.item()) == 0
+        ref = eager[key]
+        ns = ref[3]
+        assert torch.equal(_bits(st.out_o[:ns]), ref[0]), f"replay {rep} ({key}): out_o"
+        assert torch.equal(_bits(st.out_lse[:ns]), ref[1]), f"replay {rep} ({key}): out_lse"
+        assert torch.equal(_bits(st.z), ref[2]), f"replay {rep} ({key}): z"
+        assert torch_equal(st.out_o[ns:], None)                        # nothing past this set's slots
