@@ -298,6 +298,29 @@ mla_status mla_online_attend_planned(const mla_geom* geom, const mla_plan_info* 
                                      float* out_lse, int64_t* part_ptr, int32_t* part_seg, uint8_t* row_src,
                                      int32_t* status, void* workspace, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate (code under HIP graph capture that must not
+ * create memory, tight serving loops, harnesses that forbid hipMalloc): the same
+ * computation as mla_online_attend_planned with the workspace replaced by a
+ * library-owned device array of MLA_NOALLOC_SCRATCH_BYTES per GPU (allocated
+ * with the library's code on each GPU and held until the process ends).  The
+ * call allocates nothing: it validates on the host, looks the array's address
+ * up once per device (hipGetSymbolAddress) and enqueues kernels.
+ *  Arguments as for mla_online_attend_planned, without workspace / ws_bytes.
+ *  A plan whose workspace needs more than MLA_NOALLOC_SCRATCH_BYTES (a chunked
+ *  plan's partials, a very large work list, or a one-chunk rotary-value plan's
+ *  lse table when out_lse is NULL) returns MLA_ERR_WORKSPACE before anything
+ *  is enqueued; one-chunk plans of the 256K workload need about 4 MB.
+ *  Every call on a GPU uses that GPU's one array, which keeps the last call's
+ *  contents (each call writes every entry before reading it): calls that
+ *  overlap on one GPU (two streams, two host threads) race and must be
+ *  serialized by the caller. */
+#define MLA_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+mla_status mla_online_attend_planned_noalloc(const mla_geom* geom, const mla_plan_info* info, const void* plan,
+                                             const int32_t* prot_rows, const int32_t* n_prot, const void* kv,
+                                             const void* q_glob, const void* q_loc, int32_t out_dtype, void* out_o,
+                                             float* out_lse, int64_t* part_ptr, int32_t* part_seg,
+                                             uint8_t* row_src, int32_t* status, void* stream);
+
 /* Step 4 with the protected set in device memory: as mla_sliced_oproj_add, with
  * |A| read from the device (clamped to [0, info->prot_cap]) and z in f32 or bf16.
  *  o_glob, o_loc  the first N*G rows of out_o and the rows after them

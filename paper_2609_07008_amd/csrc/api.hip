@@ -18,6 +18,10 @@
 #include "protect.h"
 #include "wb.h"
 
+// Device scratch of mla_online_attend_planned_noalloc (one copy per GPU, for the
+// life of the process); host code reaches it only through scratch_address().
+static __device__ __align__(256) unsigned char scratch[MLA_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 thread_local std::string g_detail;
@@ -715,6 +719,38 @@ mla_status static_plan(const mla_geom* g, const mla_segment* segs, int32_t n_seg
   return MLA_OK;
 }
 
+// Scratch of the allocation-free attend entry point: one array per GPU, held
+// until the process ends.  In host code `scratch` names a host-side stand-in,
+// not device memory, so kernels get the device address that
+// hipGetSymbolAddress returns for the current device (looked up once per
+// device, then kept).  Every call on a GPU shares that GPU's array, and the
+// plan kernels write each entry before it is read, so nothing needs clearing.
+constexpr size_t kScratchBytes = MLA_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// device address of this GPU's scratch array (looked up on the first call on
+// each device, with that device current)
+mla_status scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(MLA_ERR_UNSUPPORTED, "device %d: the scratch table holds %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (scratch)");
+    if (p == nullptr || (reinterpret_cast<uintptr_t>(p) & 255u) != 0)
+      return fail(MLA_ERR_HIP, "scratch array at %p is not 256-byte aligned", p);
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MLA_OK;
+}
+
 // the checks shared by the two planned calls
 mla_status check_planned(const mla_geom* geom, const mla_plan_info* info) {
   if (geom == nullptr || info == nullptr) return fail(MLA_ERR_NULL, "geom and info are required");
@@ -748,18 +784,21 @@ mla_status mla_online_plan(const mla_geom* geom, const mla_segment* segs, int32_
   return upload_plan(p, plan, reinterpret_cast<hipStream_t>(stream));
 }
 
-mla_status mla_online_attend_planned(const mla_geom* geom, const mla_plan_info* info, const void* plan,
-                                     const int32_t* prot_rows, const int32_t* n_prot, const void* kv,
-                                     const void* q_glob, const void* q_loc, int32_t out_dtype, void* out_o,
-                                     float* out_lse, int64_t* part_ptr, int32_t* part_seg, uint8_t* row_src,
-                                     int32_t* status, void* workspace, size_t ws_bytes, void* stream) {
-  g_detail.clear();
+namespace {
+
+// The body of both planned attend entry points.  use_scratch: the workspace is
+// the library's per-device scratch array (workspace / ws_bytes are ignored).
+mla_status attend_planned_impl(const mla_geom* geom, const mla_plan_info* info, const void* plan,
+                               const int32_t* prot_rows, const int32_t* n_prot, const void* kv, const void* q_glob,
+                               const void* q_loc, int32_t out_dtype, void* out_o, float* out_lse, int64_t* part_ptr,
+                               int32_t* part_seg, uint8_t* row_src, int32_t* status, void* workspace,
+                               size_t ws_bytes, void* stream, bool use_scratch) {
   mla_status st = check_planned(geom, info);
   if (st != MLA_OK) return st;
   const int G = geom->n_groups, hpg = geom->n_heads / geom->n_groups;
   const int64_t* L = info->layout;
   if (plan == nullptr || n_prot == nullptr || kv == nullptr || q_glob == nullptr || out_o == nullptr ||
-      workspace == nullptr)
+      (!use_scratch && workspace == nullptr))
     return fail(MLA_ERR_NULL, "plan, n_prot, kv, q_glob, out_o and workspace are required");
   if (info->prot_cap > 0 && prot_rows == nullptr) return fail(MLA_ERR_NULL, "prot_rows is NULL");
   if (info->prot_cap > 0 && hpg > 1 && q_loc == nullptr) return fail(MLA_ERR_NULL, "q_loc is NULL but Local heads exist");
@@ -767,10 +806,20 @@ mla_status mla_online_attend_planned(const mla_geom* geom, const mla_plan_info* 
   if (out_dtype != MLA_BF16 && out_dtype != MLA_F32) return fail(MLA_ERR_SHAPE, "out_dtype %d", out_dtype);
   if (!aligned16(kv) || !aligned16(q_glob) || (q_loc && !aligned16(q_loc)) || !aligned16(out_o))
     return fail(MLA_ERR_SHAPE, "kv, q_glob, q_loc and out_o must be 16-byte aligned");
-  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 || (reinterpret_cast<uintptr_t>(plan) & 255u) != 0)
-    return fail(MLA_ERR_SHAPE, "plan and workspace must be 256-byte aligned");
-  if (ws_bytes < info->ws_bytes)
-    return fail(MLA_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, info->ws_bytes);
+  if ((reinterpret_cast<uintptr_t>(plan) & 255u) != 0) return fail(MLA_ERR_SHAPE, "plan must be 256-byte aligned");
+  if (use_scratch) {
+    // a one-chunk plan's lse table sits last in the workspace and is used only
+    // when the caller passes no out_lse
+    const size_t need = (L[W_LSE] >= 0 && out_lse != nullptr) ? (size_t)L[W_LSE] : info->ws_bytes;
+    if (need > kScratchBytes)
+      return fail(MLA_ERR_WORKSPACE, "this plan needs %zu bytes of scratch; the library's scratch array holds %zu",
+                  need, kScratchBytes);
+    if ((st = scratch_address(&workspace)) != MLA_OK) return st;
+  } else {
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return fail(MLA_ERR_SHAPE, "workspace must be 256-byte aligned");
+    if (ws_bytes < info->ws_bytes)
+      return fail(MLA_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, info->ws_bytes);
+  }
 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const unsigned char* P = reinterpret_cast<const unsigned char*>(plan);
@@ -850,6 +899,28 @@ mla_status mla_online_attend_planned(const mla_geom* geom, const mla_plan_info* 
     if (e != hipSuccess) return hip_fail(e, "merge kernel");
   }
   return MLA_OK;
+}
+
+}  // namespace
+
+mla_status mla_online_attend_planned(const mla_geom* geom, const mla_plan_info* info, const void* plan,
+                                     const int32_t* prot_rows, const int32_t* n_prot, const void* kv,
+                                     const void* q_glob, const void* q_loc, int32_t out_dtype, void* out_o,
+                                     float* out_lse, int64_t* part_ptr, int32_t* part_seg, uint8_t* row_src,
+                                     int32_t* status, void* workspace, size_t ws_bytes, void* stream) {
+  g_detail.clear();
+  return attend_planned_impl(geom, info, plan, prot_rows, n_prot, kv, q_glob, q_loc, out_dtype, out_o, out_lse,
+                             part_ptr, part_seg, row_src, status, workspace, ws_bytes, stream, false);
+}
+
+mla_status mla_online_attend_planned_noalloc(const mla_geom* geom, const mla_plan_info* info, const void* plan,
+                                             const int32_t* prot_rows, const int32_t* n_prot, const void* kv,
+                                             const void* q_glob, const void* q_loc, int32_t out_dtype, void* out_o,
+                                             float* out_lse, int64_t* part_ptr, int32_t* part_seg,
+                                             uint8_t* row_src, int32_t* status, void* stream) {
+  g_detail.clear();
+  return attend_planned_impl(geom, info, plan, prot_rows, n_prot, kv, q_glob, q_loc, out_dtype, out_o, out_lse,
+                             part_ptr, part_seg, row_src, status, nullptr, 0, stream, true);
 }
 
 mla_status mla_sliced_oproj_add_planned(const mla_geom* geom, const mla_plan_info* info, const void* o_glob,

@@ -20,7 +20,8 @@ MLA_BF16, MLA_F32 = 0, 1
 STATUS = {0: "MLA_OK", 1: "MLA_ERR_NULL", 2: "MLA_ERR_SHAPE", 3: "MLA_ERR_UNSUPPORTED",
           4: "MLA_ERR_SEGMENTS", 5: "MLA_ERR_ROWS", 6: "MLA_ERR_WORKSPACE", 7: "MLA_ERR_HIP"}
 EXPORTS = ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
-           "mla_online_plan_query", "mla_online_plan", "mla_online_attend_planned", "mla_sliced_oproj_add_planned",
+           "mla_online_plan_query", "mla_online_plan", "mla_online_attend_planned",
+           "mla_online_attend_planned_noalloc", "mla_sliced_oproj_add_planned",
            "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query", "mla_protected_rows",
            "mla_moe_fanout", "mla_shared_wb", "mla_status_str", "mla_last_error_detail", "mla_version")
 
@@ -71,6 +72,7 @@ def _load(path: str = LIB_PATH):
     lib.mla_online_plan_query.argtypes = [GP, SP, I32, I64, I32, IP]
     lib.mla_online_plan.argtypes = [GP, SP, I32, I64, I32, IP, P, SZ, P]
     lib.mla_online_attend_planned.argtypes = [GP, IP, P, P, P, P, P, P, I32, P, P, P, P, P, P, P, SZ, P]
+    lib.mla_online_attend_planned_noalloc.argtypes = [GP, IP, P, P, P, P, P, P, I32, P, P, P, P, P, P, P]
     lib.mla_sliced_oproj_add_planned.argtypes = [GP, IP, P, P, P, P, P, P, P, I32, P, P]
     lib.mla_offline_produce_query.argtypes = [GP, SP, I32, ctypes.POINTER(SZ)]
     lib.mla_offline_produce.argtypes = [GP, SP, I32, P, P, P, P, I32, P, P, SZ, P]
@@ -80,7 +82,7 @@ def _load(path: str = LIB_PATH):
     lib.mla_shared_wb.argtypes = [I64, I32, I32, P, P, I32, P, P]
     for f in ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
               "mla_online_plan_query", "mla_online_plan", "mla_online_attend_planned",
-              "mla_sliced_oproj_add_planned", "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query",
+              "mla_online_attend_planned_noalloc", "mla_sliced_oproj_add_planned", "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query",
               "mla_protected_rows", "mla_moe_fanout", "mla_shared_wb"):
         getattr(lib, f).restype = ctypes.c_int
     lib.mla_status_str.argtypes = [ctypes.c_int]
@@ -204,6 +206,21 @@ def online_attend_planned(geom, info, plan, prot_rows, n_prot, kv, q_glob, q_loc
                                          _ptr(out_lse), _ptr(part_ptr), _ptr(part_seg), _ptr(row_src), _ptr(status),
                                          _ptr(workspace), workspace.numel() * workspace.element_size(),
                                          _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20   # MLA_NOALLOC_SCRATCH_BYTES
+
+
+def online_attend_planned_noalloc(geom, info, plan, prot_rows, n_prot, kv, q_glob, q_loc, out_o, out_lse=None,
+                                  part_ptr=None, part_seg=None, row_src=None, status=None, stream=None):
+    """mla_online_attend_planned_noalloc: as online_attend_planned, with the
+    library's per-GPU scratch array in place of a workspace (nothing allocated)."""
+    g = make_geom(geom)
+    out = MLA_BF16 if out_o.dtype == torch.bfloat16 else MLA_F32
+    _check(LIB.mla_online_attend_planned_noalloc(ctypes.byref(g), ctypes.byref(info), _ptr(plan), _ptr(prot_rows),
+                                                 _ptr(n_prot), _ptr(kv), _ptr(q_glob), _ptr(q_loc), out, _ptr(out_o),
+                                                 _ptr(out_lse), _ptr(part_ptr), _ptr(part_seg), _ptr(row_src),
+                                                 _ptr(status), _stream(stream)))
 
 
 def sliced_oproj_add_planned(geom, info, o_glob, o_loc, glob_head, prot_rows, n_prot, w_o, z_off, z, stream=None):

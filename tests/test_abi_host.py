@@ -388,3 +388,17 @@ def test_planned_calls_check_the_plan_first(mla):
     other = mla.make_geom(_geom(wl, softmax_scale=0.5))
     assert attend(other, info) == 2 and oproj(other, info) == 2
     assert "geometry" in mla.LIB.mla_last_error_detail().decode()
+
+
+def test_noalloc_refuses_a_plan_larger_than_its_scratch(mla):
+    """Checked on the host before the scratch array is looked up: the device
+    pointers below are aligned placeholders that are never dereferenced."""
+    import ctypes
+    wl = make_workload(2)
+    info = mla.plan_query(wl.geom, wl.segs, 0, wl.n_prot)      # per-segment partials: GBs of workspace
+    assert info.ws_bytes > mla.NOALLOC_SCRATCH_BYTES
+    g = mla.make_geom(wl.geom)
+    fake = ctypes.c_void_p(1 << 20)
+    st = mla.LIB.mla_online_attend_planned_noalloc(ctypes.byref(g), ctypes.byref(info), fake, fake, fake, fake, fake,
+                                                   fake, 0, fake, None, None, None, None, None, None)
+    assert st == 6 and "scratch" in mla.LIB.mla_last_error_detail().decode()
