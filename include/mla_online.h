@@ -21,18 +21,23 @@
  *
  * Conventions (all entry points):
  *  - Host arrays are read during the call only.  Device arrays are owned by the
- *    caller; the library allocates no device memory (scratch comes in as a
- *    caller-provided workspace) and keeps no per-call state.
+ *    caller; the library allocates no device memory of its own beyond one
+ *    fixed scratch array per GPU used only by mla_online_attend_planned_noalloc
+ *    (everything else takes a caller-provided workspace) and keeps no per-call
+ *    state.
  *  - All device work is enqueued on `stream` (a hipStream_t passed as void*;
- *    NULL is the default stream) in call order; nothing is synchronized.  The
- *    attend, producer and protected-set calls copy a small plan (segment tables
- *    and the work list) from a library-owned pinned host buffer into the
- *    workspace on the same stream.
- *  - HIP graph capture: the merge, o-proj, W_b and MoE calls enqueue kernels
- *    only (no memset or memcpy nodes) and may be captured.  The three calls that
- *    upload a plan return MLA_ERR_UNSUPPORTED on a capturing stream, before
- *    enqueueing anything: their staging buffer is reused by later calls, so a
- *    replay would not read the plan of the captured call.
+ *    NULL is the default stream) in call order.  The host-plan attend,
+ *    producer, protected-set and mla_online_plan calls copy a plan (segment
+ *    tables and, for the first three, the work list) from a library-owned
+ *    pinned host buffer of two slots per device on the same stream; reusing a
+ *    slot waits for the copy that last read it, so a third back-to-back call
+ *    may block the host until the first call's copy has run.  Every other
+ *    call only enqueues kernels and never blocks.
+ *  - HIP graph capture: the merge, o-proj, W_b, MoE and the two planned step
+ *    calls enqueue kernels only (no memset or memcpy nodes) and may be
+ *    captured.  The calls that upload a plan return MLA_ERR_UNSUPPORTED on a
+ *    capturing stream, before enqueueing anything: their staging buffer is
+ *    reused by later calls, so a replay would not read the captured plan.
  *  - Every entry point validates its arguments on the host before enqueueing
  *    anything and returns a status; it never aborts and never falls back to a
  *    different computation.  mla_last_error_detail() describes the last failure
@@ -289,6 +294,8 @@ mla_status mla_online_plan(const mla_geom* geom, const mla_segment* segs, int32_
  *  status     device int32 [1] or NULL: MLA_OK, or MLA_ERR_ROWS when the device
  *             list was rejected (|A| > prot_cap or < 0, a row outside [0, N), not
  *             strictly increasing); the call then writes no output row
+ *             (MLA_ERR_WORKSPACE would mean the plan's bounds were exceeded,
+ *             which they cannot be for a list of at most prot_cap rows)
  *  workspace  device, 256-byte aligned, info->ws_bytes; overwritten
  * Host errors (nothing enqueued): NULL, SHAPE (also a geometry or info that does
  * not match), WORKSPACE, HIP. */
