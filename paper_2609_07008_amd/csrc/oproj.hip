@@ -81,26 +81,39 @@ void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
   const int64_t acol = PASS == 0 ? (int64_t)pg * gpp * (hpg - 1) * DC : (int64_t)pg * gpp * DC;
   const uint16_t* W = (const uint16_t*)a.w_o + (int64_t)pg * heads_pp * DC * cw;
 
-  for (int i = tid; i < OP_BM; i += NT) {
-    const int64_t m = m0 + i;
-    int flag = 0, orow = -1;
-    if (m < M) {
-      if (PASS == 0) {
+  if (PASS == 0) {
+    for (int i = tid; i < OP_BM; i += NT) {
+      const int64_t m = m0 + i;
+      int orow = -1;
+      if (m < M) {
         orow = a.prot_rows[m];
         if (orow < 0 || orow >= a.n_rows) orow = -1;   // outside z: the row is skipped
-        flag = 1;
-      } else {
-        orow = (int)m;
-        int lo = 0, hi = n_prot;            // binary search in the sorted protected rows
-        while (lo < hi) {
-          const int mid = (lo + hi) >> 1;
-          if (a.prot_rows[mid] < (int)m) lo = mid + 1; else hi = mid;
-        }
-        flag = (lo < n_prot && a.prot_rows[lo] == (int)m) ? 1 : 0;
       }
+      row_flag[i] = 1;
+      row_out[i] = orow;
     }
-    row_flag[i] = flag;
-    row_out[i] = orow;
+  } else {
+    // the tile's rows are [m0, m0 + BM): the protected ones are the run of the
+    // sorted list between two lower bounds, found once per workgroup
+    __shared__ int run[2];
+    if (tid < 2) {
+      const int64_t key = tid == 0 ? (int64_t)m0 : (int64_t)m0 + OP_BM;
+      int lo = 0, hi = n_prot;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if ((int64_t)a.prot_rows[mid] < key) lo = mid + 1; else hi = mid;
+      }
+      run[tid] = lo;
+    }
+    for (int i = tid; i < OP_BM; i += NT) {
+      row_flag[i] = 0;
+      row_out[i] = m0 + i < M ? m0 + i : -1;
+    }
+    __syncthreads();
+    for (int k = run[0] + tid; k < run[1]; k += NT) {
+      const int64_t r = (int64_t)a.prot_rows[k] - m0;
+      if (r >= 0 && r < OP_BM) row_flag[r] = 1;   // in range for any list, sorted or not
+    }
   }
 
   // weight row of K index k (k is a multiple of 32 inside one head block)
@@ -203,25 +216,38 @@ void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
   }
 
   // epilogue: the accumulators hold the transposed blocks, so a lane holds output
-  // row l32 of each 32-row block and channels half*4 + 8i .. +3 of each 32-channel block
+  // row l32 of each 32-row block and channels half*4 + 8i .. +3 of each
+  // 32-channel block.  Each 32 x 32 block goes through this wave's part of the
+  // (now idle) A buffer and comes back row-contiguous: 8 lanes cover one row's
+  // 32 channels, so every z store instruction writes eight whole 128-byte lines
+  // of f32 z (and each z_off read takes eight 64-byte runs).
+  constexpr int SLD = 36;   // staged row: 32 floats + 4 of padding
+  static_assert(NT / 64 * 32 * SLD * 4 <= OP_BM * OP_ALD * 2, "epilogue staging fits the A buffer");
+  // lane quantities recomputed here rather than kept live across the K loop
+  const int elane = (int)__lane_id();
+  float MLA_LDS* stage = (float MLA_LDS*)As + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) * (32 * SLD);
   const uint16_t* zoff = (const uint16_t*)a.z_off;
+  const int prow = elane >> 3, pc4 = (elane & 7) * 4;   // read-back: row prow + 8p, channels pc4 .. +3
 #pragma unroll
-  for (int mi = 0; mi < MI; ++mi) {
-    const int r = wm * TM + mi * 32 + l32;   // this lane's tile row
-    if (m0 + r >= M) continue;
-    const int64_t orow = row_out[r];
-    if (PASS == 0 && orow < 0) continue;
-    const int flag = row_flag[r];
+  for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < NI; ++ni)
+    for (int ni = 0; ni < NI; ++ni) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int n = n0 + wn * TN + ni * 32 + half * 4 + 8 * i;   // 4 consecutive channels
-        if (n >= cw) continue;                                     // cw is a multiple of 32
+      for (int i = 0; i < 4; ++i)
+        *(f32x4 MLA_LDS*)(stage + (elane & 31) * SLD + (elane >> 5) * 4 + 8 * i) =
+            f32x4{acc[mi][ni][4 * i], acc[mi][ni][4 * i + 1], acc[mi][ni][4 * i + 2], acc[mi][ni][4 * i + 3]};
+      const int n = n0 + wn * TN + ni * 32 + pc4;   // 4 consecutive channels; cw is a multiple of 32
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int rr = p * 8 + prow;
+        f32x4 v = *(const f32x4 MLA_LDS*)(stage + rr * SLD + pc4);
+        const int r = wm * TM + mi * 32 + rr;       // tile row
+        if (m0 + r >= M || n >= cw) continue;
+        const int64_t orow = row_out[r];
+        if (PASS == 0 && orow < 0) continue;
         const int64_t off = orow * a.d_model + (int64_t)pg * cw + n;
-        f32x4 v = {acc[mi][ni][4 * i], acc[mi][ni][4 * i + 1], acc[mi][ni][4 * i + 2], acc[mi][ni][4 * i + 3]};
         if (PASS == 1) {
-          if (flag) {
+          if (row_flag[r]) {
             if (hpg > 1) {   // the Local pass wrote this row first
               if (a.z_bf16) {
                 const u32x2 zl = *(const u32x2*)((const uint16_t*)a.z + off);
@@ -240,7 +266,7 @@ void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
         else
           *(f32x4*)(a.z + off) = v;
       }
-  }
+    }
 }
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(u32x4* p, int64_t n16) {
