@@ -33,9 +33,9 @@
  *    slot waits for the copy that last read it, so a third back-to-back call
  *    may block the host until the first call's copy has run.  Every other
  *    call only enqueues kernels and never blocks.
- *  - HIP graph capture: the merge, o-proj, W_b, MoE and the two planned step
- *    calls enqueue kernels only (no memset or memcpy nodes) and may be
- *    captured.  The calls that upload a plan return MLA_ERR_UNSUPPORTED on a
+ *  - HIP graph capture: the merge, o-proj, W_b, MoE and the planned
+ *    protected-set, attend and o-proj calls enqueue kernels only (no memset or
+ *    memcpy nodes) and may be captured.  The calls that upload a plan return MLA_ERR_UNSUPPORTED on a
  *    capturing stream, before enqueueing anything: their staging buffer is
  *    reused by later calls, so a replay would not read the captured plan.
  *  - Every entry point validates its arguments on the host before enqueueing
@@ -419,6 +419,24 @@ mla_status mla_protected_rows(const mla_segment* segs, int32_t n_segs, const mla
                               const uint8_t* row_flags, const float* index_scores,
                               int32_t* prot_rows, int32_t* n_prot, void* workspace, size_t ws_bytes,
                               void* stream);
+
+/* The protected set on the plan-once path: the same set as mla_protected_rows,
+ * with the segment table read from a plan built by mla_online_plan (it holds
+ * the storage-ordered table), so the call only enqueues kernels (its control
+ * words are cleared by a kernel, not uploaded) and may be captured in a HIP
+ * graph together with mla_online_attend_planned, which takes its prot_rows and
+ * n_prot directly (Alg. 2: ProtectedRows, then SelectiveMLA in the same layer).
+ *  info, plan     a plan from mla_online_plan (host description, device image);
+ *                 query_seg indexes the plan's segment table
+ *  cfg, row_flags, index_scores, prot_rows [N], n_prot   as for mla_protected_rows
+ *  workspace      device, 256-byte aligned, mla_protected_rows_planned_query bytes
+ *                 (17 B per row plus 16.6 KB)
+ * Errors: NULL, SHAPE (also an info not written by mla_online_plan), WORKSPACE, HIP. */
+mla_status mla_protected_rows_planned_query(const mla_plan_info* info, size_t* ws_bytes);
+
+mla_status mla_protected_rows_planned(const mla_plan_info* info, const void* plan, const mla_protect_cfg* cfg,
+                                      const uint8_t* row_flags, const float* index_scores, int32_t* prot_rows,
+                                      int32_t* n_prot, void* workspace, size_t ws_bytes, void* stream);
 
 /* ----------------------------------------------------------------------------
  * mla_moe_fanout -- the adaptive MoE fanout of Sec. 2.4 (eq:moe) for the

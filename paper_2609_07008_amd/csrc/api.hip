@@ -556,6 +556,7 @@ namespace {
 enum {
   P_SEGS, P_RANK, P_STORAGE, P_CHUNKS, P_THETA, P_GROUPS, N_ITEM_GROUPS, GLOBAL_PARTS,
   W_DYN, W_SEG_LO, W_SEG_CNT, W_SEG_BASE, W_GROUP_BASE, W_ITEMS, W_PART_PTR, W_PART_O, W_PART_LSE, W_LSE,
+  P_TKV, P_TLEN, P_TREQ, P_TORIG,   // the segment table in storage order, for the protected set
   LAYOUT_USED
 };
 static_assert(LAYOUT_USED <= 24, "mla_plan_info::layout holds 24 entries");
@@ -683,6 +684,10 @@ mla_status static_plan(const mla_geom* g, const mla_segment* segs, int32_t n_seg
   L[P_CHUNKS] = take(sizeof(mla::ChunkInfo) * T.chunks.size());
   L[P_THETA] = take(sizeof(double) * mla::kMaxRopePairs);
   L[P_GROUPS] = take(sizeof(mla::ItemGroup) * std::max<size_t>(out->groups.size(), 1));
+  L[P_TKV] = take(sizeof(int64_t) * n_segs);
+  L[P_TLEN] = take(sizeof(int64_t) * n_segs);
+  L[P_TREQ] = take(sizeof(int64_t) * n_segs);
+  L[P_TORIG] = take(sizeof(int32_t) * n_segs);
   L[N_ITEM_GROUPS] = (int64_t)out->groups.size();
   L[GLOBAL_PARTS] = T.global_parts;
   info->plan_bytes = off;
@@ -716,6 +721,13 @@ mla_status static_plan(const mla_geom* g, const mla_segment* segs, int32_t n_seg
   rope_theta_rev(g, reinterpret_cast<double*>(B + L[P_THETA]));
   if (!out->groups.empty())
     std::memcpy(B + L[P_GROUPS], out->groups.data(), sizeof(mla::ItemGroup) * out->groups.size());
+  for (int32_t i = 0; i < n_segs; ++i) {
+    const mla_segment& sg = segs[T.storage[i]];
+    reinterpret_cast<int64_t*>(B + L[P_TKV])[i] = sg.kv_start;
+    reinterpret_cast<int64_t*>(B + L[P_TLEN])[i] = sg.length;
+    reinterpret_cast<int64_t*>(B + L[P_TREQ])[i] = sg.req_offset;
+    reinterpret_cast<int32_t*>(B + L[P_TORIG])[i] = T.storage[i];
+  }
   return MLA_OK;
 }
 
@@ -1173,6 +1185,8 @@ mla_status mla_protected_rows(const mla_segment* segs, int32_t n_segs, const mla
   if ((st = upload_plan(L.table, workspace, s)) != MLA_OK) return st;
   mla::ProtectArgs a{};
   a.ws = reinterpret_cast<unsigned char*>(workspace);
+  a.table = a.ws;
+  a.zero_ctl = 0;
   a.row_flags = row_flags;
   a.scores = index_scores;
   a.prot_rows = prot_rows;
@@ -1194,6 +1208,90 @@ mla_status mla_protected_rows(const mla_segment* segs, int32_t n_segs, const mla
   a.edge_rows = cfg->edge_rows;
   a.budget = cfg->budget;
   const hipError_t e = mla::launch_protect(a, s);
+  if (e != hipSuccess) return hip_fail(e, "protected-row kernels");
+  return MLA_OK;
+}
+
+namespace {
+
+// workspace of the planned protected-set call: control words, histogram, keys,
+// flags, the gather list and the block counts (the table stays in the plan)
+size_t protect_planned_layout(int64_t N, int64_t* off_ctl, int64_t* off_hist, int64_t* off_key,
+                              int64_t* off_flag, int64_t* off_list, int64_t* off_bcnt) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, 256);
+    return (int64_t)o;
+  };
+  *off_ctl = take(mla::kProtectCtlBytes);
+  *off_hist = take(mla::kProtectHistBytes);
+  *off_key = take(sizeof(uint64_t) * (size_t)N);
+  *off_flag = take((size_t)N);
+  *off_list = take(sizeof(uint64_t) * (size_t)N);
+  *off_bcnt = take(sizeof(uint64_t) * (size_t)std::max<int64_t>(1, mla::protect_count_blocks(N)));
+  return off;
+}
+
+mla_status check_plan_info(const mla_plan_info* info) {
+  if (info == nullptr) return fail(MLA_ERR_NULL, "info is NULL");
+  if (info->check != info_checksum(info))
+    return fail(MLA_ERR_SHAPE, "info was not written by mla_online_plan (or was changed since)");
+  return MLA_OK;
+}
+
+}  // namespace
+
+mla_status mla_protected_rows_planned_query(const mla_plan_info* info, size_t* ws_bytes) {
+  g_detail.clear();
+  const mla_status st = check_plan_info(info);
+  if (st != MLA_OK) return st;
+  if (ws_bytes == nullptr) return fail(MLA_ERR_NULL, "ws_bytes is NULL");
+  int64_t o[6];
+  *ws_bytes = protect_planned_layout(info->n_rows, &o[0], &o[1], &o[2], &o[3], &o[4], &o[5]);
+  return MLA_OK;
+}
+
+mla_status mla_protected_rows_planned(const mla_plan_info* info, const void* plan, const mla_protect_cfg* cfg,
+                                      const uint8_t* row_flags, const float* index_scores, int32_t* prot_rows,
+                                      int32_t* n_prot, void* workspace, size_t ws_bytes, void* stream) {
+  g_detail.clear();
+  mla_status st = check_plan_info(info);
+  if (st != MLA_OK) return st;
+  if (cfg == nullptr) return fail(MLA_ERR_NULL, "cfg is NULL");
+  if (cfg->query_seg < -1 || cfg->query_seg >= info->n_segs)
+    return fail(MLA_ERR_SHAPE, "query_seg %d outside [-1, %d)", cfg->query_seg, info->n_segs);
+  if (cfg->edge_rows < 0 || cfg->tail_rows < 0)
+    return fail(MLA_ERR_SHAPE, "edge_rows %d and tail_rows %lld must be >= 0", cfg->edge_rows,
+                (long long)cfg->tail_rows);
+  if (!(cfg->budget >= 0.0 && cfg->budget <= 1.0)) return fail(MLA_ERR_SHAPE, "budget must lie in [0, 1]");
+  if (plan == nullptr || prot_rows == nullptr || n_prot == nullptr || workspace == nullptr)
+    return fail(MLA_ERR_NULL, "plan, prot_rows, n_prot and workspace are required");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 || (reinterpret_cast<uintptr_t>(plan) & 255u) != 0)
+    return fail(MLA_ERR_SHAPE, "plan and workspace must be 256-byte aligned");
+  mla::ProtectArgs a{};
+  const size_t need = protect_planned_layout(info->n_rows, &a.off_ctl, &a.off_hist, &a.off_key, &a.off_flag,
+                                             &a.off_list, &a.off_bcnt);
+  if (ws_bytes < need) return fail(MLA_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, need);
+  const int64_t* L = info->layout;
+  a.ws = reinterpret_cast<unsigned char*>(workspace);
+  a.table = reinterpret_cast<const unsigned char*>(plan);
+  a.zero_ctl = 1;
+  a.off_kv = L[P_TKV];
+  a.off_len = L[P_TLEN];
+  a.off_req = L[P_TREQ];
+  a.off_orig = L[P_TORIG];
+  a.row_flags = row_flags;
+  a.scores = index_scores;
+  a.prot_rows = prot_rows;
+  a.n_prot = n_prot;
+  a.n_rows = info->n_rows;
+  a.tail_rows = cfg->tail_rows;
+  a.n_segs = info->n_segs;
+  a.query_seg = cfg->query_seg;
+  a.edge_rows = cfg->edge_rows;
+  a.budget = cfg->budget;
+  const hipError_t e = mla::launch_protect(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "protected-row kernels");
   return MLA_OK;
 }

@@ -12,7 +12,8 @@
 // largest keys", and the k-th largest key kth decides every row by one compare.
 //
 // Six kernels on the caller's stream (back-to-back launches; the workspace's
-// control words and 4096-bin histogram arrive zeroed with the table upload):
+// control words and 4096-bin histogram arrive zeroed with the table upload, or,
+// when the table comes from a plan image, are zeroed by a fill kernel first):
 //   classify  (grid)  per row: its segment (binary search in the storage-ordered
 //                     table, held in LDS when it has at most 1024 segments, then
 //                     a forward walk over a thread's 8 consecutive rows), the
@@ -140,10 +141,10 @@ __global__ __launch_bounds__(256) void protect_classify_kernel(ProtectArgs a) {
   __shared__ int64_t s_kv[kLdsSegs], s_len[kLdsSegs], s_req[kLdsSegs];
   __shared__ int32_t s_orig[kLdsSegs];
   __shared__ unsigned long long cnt[3];
-  const int64_t* g_kv = (const int64_t*)(a.ws + a.off_kv);
-  const int64_t* g_len = (const int64_t*)(a.ws + a.off_len);
-  const int64_t* g_req = (const int64_t*)(a.ws + a.off_req);
-  const int32_t* g_orig = (const int32_t*)(a.ws + a.off_orig);
+  const int64_t* g_kv = (const int64_t*)(a.table + a.off_kv);
+  const int64_t* g_len = (const int64_t*)(a.table + a.off_len);
+  const int64_t* g_req = (const int64_t*)(a.table + a.off_req);
+  const int32_t* g_orig = (const int32_t*)(a.table + a.off_orig);
   const bool in_lds = a.n_segs <= kLdsSegs;
   for (int i = threadIdx.x; i < kBins; i += 256) hist[i] = 0;
   if (in_lds) {
@@ -394,9 +395,21 @@ __global__ __launch_bounds__(256) void protect_write_kernel(ProtectArgs a) {
 
 int64_t protect_count_blocks(int64_t n_rows) { return std::max<int64_t>(1, (n_rows + kRowsPerBlock - 1) / kRowsPerBlock); }
 
+__global__ __launch_bounds__(256) void protect_zero_kernel(ProtectArgs a) {
+  // the control words (kProtectCtlBytes) and the histogram (kProtectHistBytes), 4 bytes a thread
+  uint32_t* ctl = (uint32_t*)(a.ws + a.off_ctl);
+  uint32_t* hist = (uint32_t*)(a.ws + a.off_hist);
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < (int)(kProtectCtlBytes / 4); i += gridDim.x * 256) ctl[i] = 0u;
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < (int)(kProtectHistBytes / 4); i += gridDim.x * 256) hist[i] = 0u;
+}
+
 hipError_t launch_protect(const ProtectArgs& a, hipStream_t s) {
   hipError_t e;
   const int64_t n = a.n_rows;
+  if (a.zero_ctl) {
+    protect_zero_kernel<<<dim3(16), dim3(256), 0, s>>>(a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   const int64_t nb = protect_count_blocks(n);
   const unsigned grid = (unsigned)std::min<int64_t>(nb, 1024);
   protect_classify_kernel<<<dim3(grid), dim3(256), 0, s>>>(a);

@@ -23,6 +23,7 @@ EXPORTS = ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", 
            "mla_online_plan_query", "mla_online_plan", "mla_online_attend_planned",
            "mla_online_attend_planned_noalloc", "mla_sliced_oproj_add_planned",
            "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query", "mla_protected_rows",
+           "mla_protected_rows_planned_query", "mla_protected_rows_planned",
            "mla_moe_fanout", "mla_shared_wb", "mla_status_str", "mla_last_error_detail", "mla_version")
 
 
@@ -78,12 +79,15 @@ def _load(path: str = LIB_PATH):
     lib.mla_offline_produce.argtypes = [GP, SP, I32, P, P, P, P, I32, P, P, SZ, P]
     lib.mla_protected_rows_query.argtypes = [SP, I32, ctypes.POINTER(SZ)]
     lib.mla_protected_rows.argtypes = [SP, I32, ctypes.POINTER(ProtectCfg), P, P, P, P, P, SZ, P]
+    lib.mla_protected_rows_planned_query.argtypes = [IP, ctypes.POINTER(SZ)]
+    lib.mla_protected_rows_planned.argtypes = [IP, P, ctypes.POINTER(ProtectCfg), P, P, P, P, P, SZ, P]
     lib.mla_moe_fanout.argtypes = [I64, I32, P, I32, I32, ctypes.c_float, P, P, P, P, P]
     lib.mla_shared_wb.argtypes = [I64, I32, I32, P, P, I32, P, P]
     for f in ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
               "mla_online_plan_query", "mla_online_plan", "mla_online_attend_planned",
-              "mla_online_attend_planned_noalloc", "mla_sliced_oproj_add_planned", "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query",
-              "mla_protected_rows", "mla_moe_fanout", "mla_shared_wb"):
+              "mla_online_attend_planned_noalloc", "mla_sliced_oproj_add_planned", "mla_offline_produce_query",
+              "mla_offline_produce", "mla_protected_rows_query", "mla_protected_rows",
+              "mla_protected_rows_planned_query", "mla_protected_rows_planned", "mla_moe_fanout", "mla_shared_wb"):
         getattr(lib, f).restype = ctypes.c_int
     lib.mla_status_str.argtypes = [ctypes.c_int]
     lib.mla_status_str.restype = ctypes.c_char_p
@@ -272,6 +276,23 @@ def protected_rows(segs, query_seg, edge_rows, tail_rows, budget, row_flags, sco
     _check(LIB.mla_protected_rows(sarr, ns, ctypes.byref(cfg), _ptr(row_flags), _ptr(scores), _ptr(prot_rows),
                                   _ptr(n_prot), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                   _stream(stream)))
+
+
+def protected_rows_planned_query(info) -> int:
+    """Host-only: workspace bytes of mla_protected_rows_planned."""
+    ws = ctypes.c_size_t()
+    _check(LIB.mla_protected_rows_planned_query(ctypes.byref(info), ctypes.byref(ws)))
+    return ws.value
+
+
+def protected_rows_planned(info, plan, query_seg, edge_rows, tail_rows, budget, row_flags, scores, prot_rows, n_prot,
+                           workspace, stream=None):
+    """mla_protected_rows_planned: the protected set with the segment table taken
+    from the plan image; kernels only."""
+    cfg = ProtectCfg(int(query_seg), int(edge_rows), int(tail_rows), float(budget))
+    _check(LIB.mla_protected_rows_planned(ctypes.byref(info), _ptr(plan), ctypes.byref(cfg), _ptr(row_flags),
+                                          _ptr(scores), _ptr(prot_rows), _ptr(n_prot), _ptr(workspace),
+                                          workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def moe_fanout(router, tau, expert_idx, expert_w, fanout, expert_count=None, top_k: int = 6, min_k: int = 3,

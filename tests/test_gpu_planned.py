@@ -310,3 +310,121 @@ def test_planned_graph_replay_follows_device_set():
         assert torch.equal(_bits(st.out_lse[:ns]), ref[1]), f"replay {rep} ({key}): out_lse"
         assert torch.equal(_bits(st.z), ref[2]), f"replay {rep} ({key}): z"
         assert torch_equal(st.out_o[ns:], None)                        # nothing past this set's slots
+
+
+@pytest.mark.parametrize("wl_kind", ["custom", "256k"])
+@pytest.mark.parametrize("budget", [0.10, 0.25])
+def test_protected_rows_planned_equals_host_call(wl_kind, budget):
+    """mla_protected_rows_planned (segment table from the plan image, control
+    words cleared by a kernel) gives the host-table call's list bit for bit, and
+    the oracle's set."""
+    import torch
+    from paper_2609_07008_amd import mla
+    if wl_kind == "custom":
+        wl = make_custom([400, 700, 257, 520], req_perm=[2, 0, 3, 1], tq=40, H=16, G=2, d_c=512, d_r=64,
+                         d_model=256, fp32=False, seed=91, prot_rows=np.zeros(0, dtype=np.int32))
+        edge, tail = 16, 256
+    else:
+        wl = make_workload(5)
+        edge, tail = 128, 32768
+    segs, n = wl.segs, wl.n_rows
+    qseg = int(np.argmax(segs[:, 2]))
+    rng = np.random.default_rng(92)
+    flags = np.zeros(n, dtype=np.uint8)
+    flags[rng.choice(n, size=max(1, n // 100), replace=False)] |= 2
+    scores = rng.standard_normal(n).astype(np.float32)
+    fl, sc = torch.from_numpy(flags).cuda(), torch.from_numpy(scores).cuda()
+    out_h = torch.full((n,), -1, dtype=torch.int32, device="cuda")
+    cnt_h = torch.zeros((1,), dtype=torch.int32, device="cuda")
+    ws_h = torch.empty(mla.protected_rows_query(segs), dtype=torch.uint8, device="cuda")
+    mla.protected_rows(segs, qseg, edge, tail, budget, fl, sc, out_h, cnt_h, ws_h)
+    info = mla.plan_query(wl.geom, segs, n, n)
+    plan = torch.empty(max(int(info.plan_bytes), 256), dtype=torch.uint8, device="cuda")
+    info = mla.online_plan(wl.geom, segs, n, n, plan)
+    ws_p = torch.empty(mla.protected_rows_planned_query(info), dtype=torch.uint8, device="cuda")
+    out_p = torch.full((n,), -1, dtype=torch.int32, device="cuda")
+    cnt_p = torch.zeros((1,), dtype=torch.int32, device="cuda")
+    for _ in range(2):   # twice on the same workspace: the control words must be cleared each call
+        mla.protected_rows_planned(info, plan, qseg, edge, tail, budget, fl, sc, out_p, cnt_p, ws_p)
+    torch.cuda.synchronize()
+    k = int(cnt_h.item())
+    assert int(cnt_p.item()) == k
+    assert torch.equal(out_p[:k], out_h[:k])
+    a_ref = M.protected_rows(segs, qseg, flags, scores, edge, tail, budget)
+    assert np.array_equal(out_p[:k].cpu().numpy(), a_ref)
+
+
+def test_serving_layer_captured_once():
+    """One layer of the serving loop captured as one HIP graph and replayed for
+    several layers: the protected set (planned call) from per-layer Indexer
+    scores, the Local-head queries of those rows gathered by torch, attention,
+    the sliced projection into a bf16 z and y = W_b z.  Each replay equals the
+    same chain run eagerly on that layer's inputs, bit for bit."""
+    import torch
+    from paper_2609_07008_amd import device_inputs, mla, step
+    kw = dict(doc_lens=[400, 700, 257, 520], req_perm=[2, 0, 3, 1], tq=40, H=16, G=2, d_c=512, d_r=64,
+              d_model=256, fp32=False, seed=93)
+    wl = make_custom(prot_rows=np.zeros(0, dtype=np.int32), **kw)
+    g = wl.geom
+    n, G, hl = wl.n_rows, g.n_groups, g.heads_per_group - 1
+    qseg = int(np.argmax(wl.segs[:, 2]))
+    rng = np.random.default_rng(94)
+    inputs = device_inputs.upload(wl)
+    # every row's Local-head queries (the caller gathers the protected ones)
+    q_all = (torch.randn((n, G, hl, g.d_latent + g.d_rope), device="cuda") * 0.05).to(torch.bfloat16)
+    w_b = (torch.randn((192, g.d_model), device="cuda") * 0.02).to(torch.bfloat16)
+    st = step.PlannedStep(g, wl.segs, wl.glob_head, n, n, z_dtype=torch.bfloat16, bookkeeping=False)
+    ws_p = torch.empty(mla.protected_rows_planned_query(st.info), dtype=torch.uint8, device="cuda")
+    flags = torch.zeros((n,), dtype=torch.uint8, device="cuda")
+    scores = torch.empty((n,), dtype=torch.float32, device="cuda")
+    prot = torch.empty((n,), dtype=torch.int32, device="cuda")
+    n_prot = torch.empty((1,), dtype=torch.int32, device="cuda")
+    y = torch.empty((n, 192), dtype=torch.float32, device="cuda")
+
+    def layer(stream=None):
+        mla.protected_rows_planned(st.info, st.plan, qseg, 16, 256, 0.2, flags, scores, prot, n_prot, ws_p,
+                                   stream=stream)
+        q_loc = torch.index_select(q_all, 0, prot.clamp(0, n - 1).long())
+        st.run(prot, n_prot, inputs["kv"], inputs["q_glob"], q_loc, inputs["w_o"], inputs["z_off"], stream=stream)
+        mla.shared_wb(st.z, w_b, y, stream=stream)
+
+    # per layer: Indexer scores, and dirty rows (1 %, 30 %: past the budget, none)
+    layers = []
+    for frac in (0.01, 0.30, 0.0):
+        fl = np.zeros(n, dtype=np.uint8)
+        fl[rng.choice(n, size=int(frac * n), replace=False)] |= 2
+        layers.append((torch.from_numpy(rng.standard_normal(n).astype(np.float32)).cuda(),
+                       torch.from_numpy(fl).cuda()))
+    eager = []
+    for sc, fl in layers:
+        scores.copy_(sc)
+        flags.copy_(fl)
+        layer()
+        torch.cuda.synchronize()
+        k = int(n_prot.item())
+        ns = n * G + k * g.n_local
+        eager.append((k, _bits(prot[:k]), _bits(st.out_o[:ns]), _bits(st.z), _bits(y)))
+    assert len({e[0] for e in eager}) >= 2          # the size of the protected set changes between layers
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        layer(stream=side)                       # warm the torch ops on the side stream
+        with torch.cuda.graph(graph, stream=side):
+            layer(stream=side)
+    torch.cuda.synchronize()
+    for rep, li in enumerate([0, 1, 2, 1, 0]):
+        scores.copy_(layers[li][0])
+        flags.copy_(layers[li][1])
+        for t in (st.out_o, st.z, y, prot):
+            t.view(torch.uint8).fill_(0xFF)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        k, p_ref, o_ref, z_ref, y_ref = eager[li]
+        assert int(n_prot.item()) == k, f"replay {rep}"
+        ns = n * G + k * g.n_local
+        assert torch.equal(_bits(prot[:k]), p_ref), f"replay {rep}: protected rows"
+        assert torch.equal(_bits(st.out_o[:ns]), o_ref), f"replay {rep}: head outputs"
+        assert torch.equal(_bits(st.z), z_ref), f"replay {rep}: z"
+        assert torch.equal(_bits(y), y_ref), f"replay {rep}: y"
