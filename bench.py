@@ -226,14 +226,23 @@ def offline_producer(wl, torch, stream, reps: int = 2, seed: int = 70080):
     args = (g, wl.segs, kv, q, wl.glob_head, w_o, mla.MLA_BF16, z, ws)
     mla.offline_produce(*args, stream=stream)
     torch.cuda.synchronize()
-    ts = []
+    # three calls back to back, as when documents are produced one after another:
+    # each call's host plan (about 4 ms at this size) overlaps the previous call's
+    # kernels, except the first call's, which is counted once in the three
+    ts, one = [], []
     for _ in range(reps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(3):
+            mla.offline_produce(*args, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) / 3e3)
         e0.record(stream)
         mla.offline_produce(*args, stream=stream)
         e1.record(stream)
         torch.cuda.synchronize()
-        ts.append(e0.elapsed_time(e1) / 1e3)
+        one.append(e0.elapsed_time(e1) / 1e3)
     t = float(np.median(ts))
     # algorithmic work: each row's Local heads attend to u+1 keys of their own segment
     keys = float(sum(int(ln) * (int(ln) + 1) // 2 for _, ln, _ in np.asarray(wl.segs)))
@@ -241,7 +250,8 @@ def offline_producer(wl, torch, stream, reps: int = 2, seed: int = 70080):
     flop_proj = n * g.n_groups * hl * 2.0 * g.d_latent * g.d_model / g.n_proj_groups
     del kv, q, w_o, z, ws
     torch.cuda.empty_cache()
-    return {"ms": round(t * 1e3, 3), "rows_per_s": round(n / t, 1), "flop": flop_attn + flop_proj,
+    return {"ms": round(t * 1e3, 3), "ms_isolated_call": round(float(np.median(one)) * 1e3, 3),
+            "rows_per_s": round(n / t, 1), "flop": flop_attn + flop_proj,
             "tflops": round((flop_attn + flop_proj) / t / 1e12, 3),
             "pct_bf16_peak": round(100 * (flop_attn + flop_proj) / t / 1e12 / PEAK_BF16_TFLOPS, 2),
             "local_head_rows": n * g.n_groups * hl, "out": "bf16 [rows, d_model]",
