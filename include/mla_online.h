@@ -94,7 +94,9 @@ typedef enum mla_dtype { MLA_BF16 = 0, MLA_F32 = 1 } mla_dtype;
  *                 segment's canonical-frame sum is rotated by R(-(t - p_s)), i.e.
  *                 RestorePhase R(+p_s) then R^{-1} = R(-t) (eq:offonline, Alg. 2).
  *                 Head outputs, partials, the merge and the W_o head blocks are
- *                 then d_v wide.                                               */
+ *                 then d_v wide.  The attention keeps each head-row's RoPE
+ *                 output sums in the workspace (64 KB per work item), which the
+ *                 size queries include.                                        */
 typedef struct mla_geom {
   int32_t n_heads;
   int32_t n_groups;
@@ -314,9 +316,10 @@ mla_status mla_online_attend_planned(const mla_geom* geom, const mla_plan_info* 
  * up once per device (hipGetSymbolAddress) and enqueues kernels.
  *  Arguments as for mla_online_attend_planned, without workspace / ws_bytes.
  *  A plan whose workspace needs more than MLA_NOALLOC_SCRATCH_BYTES (a chunked
- *  plan's partials, a very large work list, or a one-chunk rotary-value plan's
- *  lse table when out_lse is NULL) returns MLA_ERR_WORKSPACE before anything
- *  is enqueued; one-chunk plans of the 256K workload need about 4 MB.
+ *  plan's partials, a very large work list, or a rotary-value plan's
+ *  accumulators beyond a few hundred work items) returns MLA_ERR_WORKSPACE
+ *  before anything is enqueued; one-chunk plans of the 256K workload with the
+ *  latent value need about 4 MB.
  *  Every call on a GPU uses that GPU's one array, which keeps the last call's
  *  contents (each call writes every entry before reading it): calls that
  *  overlap on one GPU (two streams, two host threads) race and must be
@@ -363,8 +366,8 @@ mla_status mla_sliced_oproj_add_planned(const mla_geom* geom, const mla_plan_inf
  *   out_dtype      MLA_BF16 or MLA_F32: element type of z_off.
  *   z_off          [N, d_model] device, written (every element).
  *   workspace      device, 256-byte aligned, at least the size returned by
- *                  mla_offline_produce_query: plan, bf16 head outputs
- *                  [N, G, hpg-1, d_v] (and their lse with a rotary value).
+ *                  mla_offline_produce_query: plan (with a rotary value its
+ *                  accumulators), bf16 head outputs [N, G, hpg-1, d_v].
  *                  Overwritten.
  * With hpg == 1 (no Local heads) z_off is written with zeros.  Errors as for
  * mla_online_attend.

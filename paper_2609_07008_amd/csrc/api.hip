@@ -129,6 +129,10 @@ struct Plan {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// rotary value: bytes of the attention kernel's accumulators, 128 f32 per
+// head-row of each of n_items work items
+int64_t rot_bytes(int64_t n_items) { return std::max<int64_t>(n_items, 1) * mla::kTileRows * 128 * 4; }
+
 // What depends only on the segment table: request order, storage order, the
 // chunking of each segment's visible list (ranks 0 .. rank(s)) and the Global
 // partial index.  offline: every segment sees only itself (Alg. 1).
@@ -304,6 +308,9 @@ mla_status build_plan(const mla_geom* g, const mla_segment* segs, int32_t n_segs
   h.off_cum_local = take(sizeof(int64_t) * (n_prot + 1));
   h.off_theta = take(sizeof(double) * mla::kMaxRopePairs);
   h.total_bytes = (int64_t)off;
+  // rotary value: the attention kernel's per-item accumulators, after the image
+  h.off_rot = g->value_rope ? (int64_t)off : -1;
+  h.ws_bytes = (int64_t)off + (g->value_rope ? rot_bytes((int64_t)items.size()) : 0);
   if (!want_blob) return MLA_OK;
 
   out->blob.assign(off, 0);
@@ -432,7 +439,7 @@ mla_status mla_online_attend_query(const mla_geom* geom, const mla_segment* segs
   if (st != MLA_OK) return st;
   *n_slots = p.hdr.n_slots;
   *n_parts = p.hdr.n_parts;
-  *ws_bytes = (size_t)p.hdr.total_bytes;
+  *ws_bytes = (size_t)p.hdr.ws_bytes;
   return MLA_OK;
 }
 
@@ -453,8 +460,8 @@ mla_status mla_online_attend(const mla_geom* geom, const mla_segment* segs, int3
   if (!aligned16(kv) || !aligned16(q_glob) || (q_loc && !aligned16(q_loc)) || !aligned16(part_o))
     return fail(MLA_ERR_SHAPE, "kv, q_glob, q_loc and part_o must be 16-byte aligned");
   if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return fail(MLA_ERR_SHAPE, "workspace must be 256-byte aligned");
-  if (ws_bytes < (size_t)p.hdr.total_bytes)
-    return fail(MLA_ERR_WORKSPACE, "workspace %zu bytes < required %lld", ws_bytes, (long long)p.hdr.total_bytes);
+  if (ws_bytes < (size_t)p.hdr.ws_bytes)
+    return fail(MLA_ERR_WORKSPACE, "workspace %zu bytes < required %lld", ws_bytes, (long long)p.hdr.ws_bytes);
 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if ((st = upload_plan(p, workspace, s)) != MLA_OK) return st;
@@ -477,6 +484,8 @@ mla_status mla_online_attend(const mla_geom* geom, const mla_segment* segs, int3
   a.scale_log2 = geom->softmax_scale * 1.4426950408889634f;
   a.local_slot_base = p.hdr.n_rows * geom->n_groups;
   a.out_direct = nullptr;
+  a.rot = p.hdr.off_rot >= 0 ? reinterpret_cast<float*>(reinterpret_cast<unsigned char*>(workspace) + p.hdr.off_rot)
+                             : nullptr;
   hipError_t e = mla::launch_plan(a, s);
   if (e != hipSuccess) return hip_fail(e, "plan kernels");
   e = mla::launch_attend(a, s);
@@ -555,7 +564,7 @@ namespace {
 // in the workspace (W_*), and two counts
 enum {
   P_SEGS, P_RANK, P_STORAGE, P_CHUNKS, P_THETA, P_GROUPS, N_ITEM_GROUPS, GLOBAL_PARTS,
-  W_DYN, W_SEG_LO, W_SEG_CNT, W_SEG_BASE, W_GROUP_BASE, W_ITEMS, W_PART_PTR, W_PART_O, W_PART_LSE, W_LSE,
+  W_DYN, W_SEG_LO, W_SEG_CNT, W_SEG_BASE, W_GROUP_BASE, W_ITEMS, W_PART_PTR, W_PART_O, W_PART_LSE, W_ROT,
   P_TKV, P_TLEN, P_TREQ, P_TORIG,   // the segment table in storage order, for the protected set
   LAYOUT_USED
 };
@@ -701,13 +710,12 @@ mla_status static_plan(const mla_geom* g, const mla_segment* segs, int32_t n_seg
   L[W_ITEMS] = take(sizeof(mla::WorkItem) * std::max<int64_t>(info->max_items, 1));
   if (info->one_chunk) {
     L[W_PART_PTR] = L[W_PART_O] = L[W_PART_LSE] = -1;
-    L[W_LSE] = g->value_rope ? take(sizeof(float) * (size_t)info->max_slots) : -1;
   } else {
     L[W_PART_PTR] = take(sizeof(int64_t) * (size_t)(info->max_slots + 1));
     L[W_PART_O] = take(sizeof(float) * (size_t)info->max_parts * dv);
     L[W_PART_LSE] = take(sizeof(float) * (size_t)info->max_parts);
-    L[W_LSE] = -1;
   }
+  L[W_ROT] = g->value_rope ? take((size_t)rot_bytes(info->max_items)) : -1;
   info->ws_bytes = off;
   info->check = info_checksum(info);
   if (!want_blob) return MLA_OK;
@@ -820,9 +828,7 @@ mla_status attend_planned_impl(const mla_geom* geom, const mla_plan_info* info, 
     return fail(MLA_ERR_SHAPE, "kv, q_glob, q_loc and out_o must be 16-byte aligned");
   if ((reinterpret_cast<uintptr_t>(plan) & 255u) != 0) return fail(MLA_ERR_SHAPE, "plan must be 256-byte aligned");
   if (use_scratch) {
-    // a one-chunk plan's lse table sits last in the workspace and is used only
-    // when the caller passes no out_lse
-    const size_t need = (L[W_LSE] >= 0 && out_lse != nullptr) ? (size_t)L[W_LSE] : info->ws_bytes;
+    const size_t need = info->ws_bytes;
     if (need > kScratchBytes)
       return fail(MLA_ERR_WORKSPACE, "this plan needs %zu bytes of scratch; the library's scratch array holds %zu",
                   need, kScratchBytes);
@@ -897,12 +903,13 @@ mla_status attend_planned_impl(const mla_geom* geom, const mla_plan_info* info, 
     a.part_ptr = part_ptr;
     a.out_direct = out_o;
     a.out_direct_bf16 = out_dtype == MLA_BF16 ? 1 : 0;
-    a.part_lse = out_lse != nullptr ? out_lse : (L[W_LSE] >= 0 ? reinterpret_cast<float*>(W + L[W_LSE]) : nullptr);
+    a.part_lse = out_lse;
   } else {
     a.part_ptr = part_ptr != nullptr ? part_ptr : reinterpret_cast<int64_t*>(W + L[W_PART_PTR]);
     a.part_o = reinterpret_cast<float*>(W + L[W_PART_O]);
     a.part_lse = reinterpret_cast<float*>(W + L[W_PART_LSE]);
   }
+  a.rot = L[W_ROT] >= 0 ? reinterpret_cast<float*>(W + L[W_ROT]) : nullptr;
   if ((e = mla::launch_plan(a, s)) != hipSuccess) return hip_fail(e, "plan kernels");
   if ((e = mla::launch_attend(a, s)) != hipSuccess) return hip_fail(e, "attention kernel");
   if (!info->one_chunk) {
@@ -990,7 +997,6 @@ struct OfflineLayout {
   Plan plan;
   std::vector<int32_t> rows;   // identity row list: every row computes its Local heads
   size_t off_o = 0;            // bf16 head outputs [N, G, hpg-1, dv]
-  size_t off_lse = 0;          // rotary value only: their lse [N, G, hpg-1] f32
   size_t total = 0;
 };
 
@@ -1007,9 +1013,8 @@ mla_status offline_layout(const mla_geom* geom, const mla_segment* segs, int32_t
   const int hpg = geom->n_heads / geom->n_groups;
   const size_t n_out = (size_t)N * geom->n_groups * (hpg - 1);
   const size_t o_bytes = n_out * head_dv(geom) * 2;
-  L->off_o = align_up((size_t)L->plan.hdr.total_bytes, 256);
-  L->off_lse = L->off_o + align_up(o_bytes, 256);
-  L->total = L->off_lse + (geom->value_rope ? align_up(n_out * 4, 256) : 0);
+  L->off_o = align_up((size_t)L->plan.hdr.ws_bytes, 256);
+  L->total = L->off_o + align_up(o_bytes, 256);
   return MLA_OK;
 }
 
@@ -1074,7 +1079,8 @@ mla_status mla_offline_produce(const mla_geom* geom, const mla_segment* segs, in
   a.local_slot_base = 0;
   a.out_direct = ws + L.off_o;
   a.out_direct_bf16 = 1;
-  a.part_lse = geom->value_rope ? reinterpret_cast<float*>(ws + L.off_lse) : nullptr;
+  a.part_lse = nullptr;
+  a.rot = L.plan.hdr.off_rot >= 0 ? reinterpret_cast<float*>(ws + L.plan.hdr.off_rot) : nullptr;
   hipError_t e = mla::launch_attend(a, s);
   if (e != hipSuccess) return hip_fail(e, "attention kernel");
 

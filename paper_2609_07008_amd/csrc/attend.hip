@@ -101,6 +101,15 @@ __device__ __forceinline__ void s_acc(f32x16& s0, f32x16& s1, const bf16x8& k0, 
       : "+v"(s0), "+v"(s1)
       : "v"(k0), "v"(k1), "v"(q));
 }
+// A rotary value's RoPE output block: r += V P for one 16-key step, in
+// architectural VGPRs for the same reason.  The compiler does not see an MFMA
+// here, so the asm carries the wait states itself: the leading s_nop covers a
+// vector ALU write of P just before (the compiler packs P's bf16 pairs lazily,
+// next to their first use), r_acc_ready a memory or vector ALU read of r after.
+__device__ __forceinline__ void r_acc1(f32x16& r, const bf16x8& v, const bf16x8& p) {
+  asm("s_nop 4\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(r) : "v"(v), "v"(p));
+}
+__device__ __forceinline__ void r_acc_ready(f32x16& r) { asm("s_nop 15\n\ts_nop 7" : "+v"(r)); }
 // 24 wait states: more than an XDL result needs before a vector ALU read
 __device__ __forceinline__ void s_acc_ready(f32x16& s0, f32x16& s1) {
   asm("s_nop 15\n\ts_nop 7" : "+v"(s0), "+v"(s1));
@@ -255,9 +264,121 @@ __device__ __forceinline__ int relocate_query(bf16x8 (&qf)[C::KS], const ItemVie
   return v.valid ? (int)lm : 0x7fffffff;
 }
 
-template <int DC, int DR>
+// A lane's share of a 64-dim RoPE output row held as two 32-dim MFMA output
+// blocks: register 4i + j of block dd is dim dd*32 + half*4 + 8i + j, so each
+// rotation pair (k, k + 32) sits in one register of the two blocks.
+__device__ __forceinline__ void rot_store(float* p, int half, const f32x16 (&r)[2]) {
+#pragma unroll
+  for (int dd = 0; dd < 2; ++dd)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *(f32x4*)(p + dd * 32 + half * 4 + 8 * i) = f32x4{r[dd][4 * i], r[dd][4 * i + 1], r[dd][4 * i + 2], r[dd][4 * i + 3]};
+}
+// tot += R(-dd*theta) acc, pair by pair: the angle reduced in double precision
+// (revolutions) and fed to the hardware sin/cos
+__device__ __forceinline__ void rot_accumulate(f32x16 (&tot)[2], const f32x16 (&acc)[2], double dd,
+                                               const double* theta_rev, int half) {
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int k = half * 4 + (e >> 2) * 8 + (e & 3);
+    const double rev = dd * theta_rev[k];
+    const float r = (float)(rev - rint(rev));
+    const float sn = __builtin_amdgcn_sinf(r), cn = __builtin_amdgcn_cosf(r);
+    const float x = acc[0][e], y = acc[1][e];
+    tot[0][e] += x * cn + y * sn;
+    tot[1][e] += y * cn - x * sn;
+  }
+}
+
+// Rotary-value accumulators of one wave in device memory, lane-major: four
+// 32-dim blocks (0, 1: the current segment's RoPE output sum, canonical frame;
+// 2, 3: the row's total, query frame), each 4 KB = four 1 KB runs, run i holding
+// registers 4i..4i+3 of every lane at 16 bytes per lane, so that each 16-byte
+// load or store of a wave is one contiguous kilobyte.  The wave's base is
+// uniform and the lane's byte offset is recomputed at each use (an opaque asm,
+// so that no 64-bit per-lane pointer is hoisted out of the tile loop and held in
+// registers): the loads and stores take the scalar-base + 32-bit offset form.
+__device__ __forceinline__ uint32_t lane_x16() {
+  uint32_t v;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0\n\tv_lshlrev_b32 %0, 4, %0" : "=v"(v));
+  return v;
+}
+__device__ __forceinline__ float* rot_run(float* w, int b, int i, uint32_t lo) {
+  return (float*)((char*)w + (uint32_t)(b * 4096 + i * 1024) + lo);
+}
+__device__ __forceinline__ float* rot_run(float* w, int b, int i) { return rot_run(w, b, i, lane_x16()); }
+__device__ __forceinline__ void rot_blk_load(float* w, int b, f32x16& r) {
+  const uint32_t lo = lane_x16();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const f32x4 x = *(const f32x4*)rot_run(w, b, i, lo);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r[4 * i + j] = x[j];
+  }
+}
+__device__ __forceinline__ void rot_blk_store(float* w, int b, const f32x16& r) {
+  const uint32_t lo = lane_x16();
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    *(f32x4*)rot_run(w, b, i, lo) = f32x4{r[4 * i], r[4 * i + 1], r[4 * i + 2], r[4 * i + 3]};
+}
+// all four blocks cleared
+__device__ __forceinline__ void rot_clear(float* w) {
+#pragma unroll
+  for (int b = 0; b < 4; ++b)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) *(f32x4*)rot_run(w, b, i) = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+// Close a segment: its sum, rotated by R(-dd*theta), added into the row's
+// total, and the sum cleared for the next segment; one run at a time, so that
+// few registers are live.  The register 4i + j of block 0 is dim
+// half*4 + 8i + j and its rotation partner (+32) the same register of block 1.
+__device__ __forceinline__ void rot_close(float* w, double dd, const double* theta_rev) {
+  const int half = (int)(__lane_id() >> 5);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const f32x4 x = *(const f32x4*)rot_run(w, 0, i), y = *(const f32x4*)rot_run(w, 1, i);
+    f32x4 tx = *(const f32x4*)rot_run(w, 2, i), ty = *(const f32x4*)rot_run(w, 3, i);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const double rev = dd * theta_rev[half * 4 + 8 * i + j];
+      const float r = (float)(rev - rint(rev));
+      const float sn = __builtin_amdgcn_sinf(r), cn = __builtin_amdgcn_cosf(r);
+      tx[j] += x[j] * cn + y[j] * sn;
+      ty[j] += y[j] * cn - x[j] * sn;
+    }
+    *(f32x4*)rot_run(w, 2, i) = tx;
+    *(f32x4*)rot_run(w, 3, i) = ty;
+    *(f32x4*)rot_run(w, 0, i) = f32x4{0.f, 0.f, 0.f, 0.f};
+    *(f32x4*)rot_run(w, 1, i) = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+}
+
+// Order of a tile's P.V MFMAs with a rotary value: the n_lat latent MFMAs in
+// order, and the 8 RoPE-block MFMAs (block b, 16-key step j) placed after latent
+// MFMA kRopeAfter[b] + 3j.  Each block's 16 accumulators are then loaded ~14
+// latent MFMAs before their first use and stored ~16 before the tile's end, and
+// only one block is in registers at a time.  code[st] of sequence step st: the
+// latent index, or -1 - (4b + j) for a RoPE step.
+constexpr int kRopeAfter[2] = {13, 37};
+template <int NLAT, bool ROT>
+struct PvOrder {
+  static constexpr int n = NLAT + (ROT ? 8 : 0);
+  int code[n];
+  constexpr PvOrder() : code() {
+    int l = 0, r = 0;
+    for (int k = 0; k < n; ++k) {
+      const bool rope = ROT && r < 8 && l == kRopeAfter[r >> 2] + 3 * (r & 3) + 1;
+      code[k] = rope ? -1 - r : l;
+      if (rope) ++r; else ++l;
+    }
+  }
+};
+
+template <int DC, int DR, bool ROT>
 __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   using C = Cfg<DC, DR>;
+  static_assert(!ROT || DR == 64, "rotation pairs (j, j + 32) sit in one lane of the two RoPE output blocks");
   __shared__ __attribute__((aligned(16))) unsigned char lds[2 * C::TILE_BYTES];
   __shared__ unsigned restart_at;
 
@@ -276,6 +397,10 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   const bool valid = v.valid, active = v.active;
   const int64_t slot = v.slot;
   const uint16_t* qsrc = v.qsrc;
+  // rotary value: the wave's accumulators in device memory (the registers are
+  // full), 16 KB per wave (rot_run); the address is recomputed from the item and
+  // wave at each use, so that it holds no register across the tile loop
+  auto rot = [&]() -> float* { return a.rot + ((int64_t)item_id * 4 + wave) * 4096; };
 
   // ---- Q fragments (B operand of S^T = K Q^T), loaded once the first tile's loads
   // are out: step ks holds dims ks*16 + half*8 .. +8; for DR == 16 the RoPE step
@@ -411,6 +536,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
     relocate(cs);
     if (restarted) issue(L, cs, n_keys, 0);   // the first attempt's went out before the queries
 
+    if (ROT && active) rot_clear(rot());
     bool restart = false;
     const bool may_vote = restart_allowed(attempt);   // uniform: the last attempt never votes
     bool first_tile = !restarted;   // uniform over the workgroup
@@ -463,9 +589,17 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
         }
         // the first V^T fragments of P.V do not depend on the softmax: read them now
         constexpr int NPV = C::PS * C::OB;
+        // rotary value: K_r^T P^T into the two RoPE output blocks, placed by pv_code
+        constexpr int NRV = ROT ? 2 * C::PS : 0;
         constexpr int VD = 3;   // V^T fragments in flight ahead of their MFMA
+        constexpr PvOrder<NPV, ROT> order{};
         auto vfrag = [&](int st) -> bf16x8 {
-          const int s2 = st / C::OB, d = st % C::OB;
+          int s2 = st / C::OB, d = st % C::OB;
+          if constexpr (ROT) {
+            const int code = order.code[st];
+            s2 = code >= 0 ? code / C::OB : (-1 - code) & 3;
+            d = code >= 0 ? code % C::OB : C::OB + ((-1 - code) >> 2);
+          }
           const int off = vb[d & 1][s2 >> 1] + (d >> 1) * 1024 + (s2 & 1) * 2 * C::KB8;
           const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((MLA_LDS bf16x4*)(buf + off));
           const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((MLA_LDS bf16x4*)(buf + off + C::KB8));
@@ -535,13 +669,29 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
         }
         l_run += rsum;   // this lane's keys only; the two halves are combined at the end
 
+        // rotary value: the segment's running RoPE output sum, one 32-dim block at a time
+        f32x16 racc;
+        if (ROT) rot_blk_load(rot(), 0, racc);
+
         // ---- O^T += V^T P^T over the 64 keys: 16-key steps outer, output blocks inner ----
 #pragma unroll
-        for (int st = 0; st < NPV; ++st) {
-          if (st + VD < NPV) vt[(st + VD) % (VD + 1)] = vfrag(st + VD);
+        for (int st = 0; st < NPV + NRV; ++st) {
+          if (st + VD < NPV + NRV) vt[(st + VD) % (VD + 1)] = vfrag(st + VD);
           __builtin_amdgcn_sched_barrier(0);
-          const int s2 = st / C::OB, d = st % C::OB;
-          o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt[st % (VD + 1)], pf[s2], o[d], 0, 0, 0);
+          const int code = ROT ? order.code[st] : st;
+          if (code >= 0) {
+            const int s2 = code / C::OB, d = code % C::OB;
+            o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt[st % (VD + 1)], pf[s2], o[d], 0, 0, 0);
+          } else {
+            const int b = (-1 - code) >> 2, j = (-1 - code) & 3;
+            r_acc1(racc, vt[st % (VD + 1)], pf[j]);
+            if (j == 3) {
+              // block b is complete: store it; block 1 is loaded into the same registers
+              r_acc_ready(racc);
+              rot_blk_store(rot(), b, racc);
+              if (b == 0) rot_blk_load(rot(), 1, racc);
+            }
+          }
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -549,6 +699,10 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
       ++ti;
       if (!more) break;
       if (n_rank != c_rank) {   // the next tile opens a new segment
+        if (ROT) {
+          // the closing segment's sum, rotated by R(-(t - p_s)), into the row's total
+          if (active) rot_close(rot(), (double)(v.t_pos - cs.req_offset), v.theta_rev);
+        }
         c_rank = n_rank;
         cs = ns;
         relocate(cs);
@@ -578,10 +732,24 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   if (!valid) return;
   const float l_tot = lx + ly;
   const float inv = 1.f / l_tot;
+  // rotary value: the last segment's sum into the row's total, normalized
+  f32x16 vr[2];
+  if (ROT) {
+    f32x16 acc[2];
+    rot_blk_load(rot(), 0, acc[0]);
+    rot_blk_load(rot(), 1, acc[1]);
+    rot_blk_load(rot(), 2, vr[0]);
+    rot_blk_load(rot(), 3, vr[1]);
+    rot_accumulate(vr, acc, (double)(v.t_pos - cs.req_offset), v.theta_rev, half);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      vr[0][e] *= inv;
+      vr[1][e] *= inv;
+    }
+  }
   if (a.out_direct != nullptr) {
     // one chunk per slot (the merge done here by online rescaling, or the
-    // offline producer): the head output itself, and its lse when asked for (a
-    // rotary value's second pass normalizes with it)
+    // offline producer): the head output itself, and its lse when asked for
     if (a.part_lse != nullptr && half == 0) a.part_lse[slot] = (m_run + __log2f(l_tot)) * 0.6931471805599453f;
     if (a.out_direct_bf16) {
       uint16_t* ob = (uint16_t*)a.out_direct + slot * a.dv;
@@ -591,6 +759,13 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
         for (int i = 0; i < 4; ++i)
           *(u32x2*)(ob + d * 32 + half * 4 + 8 * i) = u32x2{pack_bf16x2(o[d][4 * i] * inv, o[d][4 * i + 1] * inv),
                                                             pack_bf16x2(o[d][4 * i + 2] * inv, o[d][4 * i + 3] * inv)};
+      if (ROT)
+#pragma unroll
+        for (int d = 0; d < 2; ++d)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            *(u32x2*)(ob + DC + d * 32 + half * 4 + 8 * i) = u32x2{pack_bf16x2(vr[d][4 * i], vr[d][4 * i + 1]),
+                                                                   pack_bf16x2(vr[d][4 * i + 2], vr[d][4 * i + 3])};
     } else {
       float* of = (float*)a.out_direct + slot * a.dv;
 #pragma unroll
@@ -599,6 +774,7 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
         for (int i = 0; i < 4; ++i)
           *(f32x4*)(of + d * 32 + half * 4 + 8 * i) =
               f32x4{o[d][4 * i] * inv, o[d][4 * i + 1] * inv, o[d][4 * i + 2] * inv, o[d][4 * i + 3] * inv};
+      if (ROT) rot_store(of + DC, half, vr);
     }
     return;
   }
@@ -611,236 +787,10 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
       f32x4 v = {o[d][4 * i] * inv, o[d][4 * i + 1] * inv, o[d][4 * i + 2] * inv, o[d][4 * i + 3] * inv};
       *(f32x4*)(dst + d * 32 + half * 4 + 8 * i) = v;
     }
+  if (ROT) rot_store(dst + DC, half, vr);
   if (half == 0) a.part_lse[pidx] = (m_run + __log2f(l_tot)) * 0.6931471805599453f;
 }
 
-
-// ----------------------------------------------------------------------------
-// Rotary value (value = the whole latent row): the RoPE part of each head
-// output.  A second pass over the same work items and tiles: S^T = K Q^T as
-// above, weights 2^(s*scale*log2e - L) with L = the partial's log2-sum-exp
-// (already normalized), and O_r^T += K_r^T P^T for the d_r RoPE dims of the
-// tile (two 32-dim output blocks of the transposing V reads).  Each segment's
-// sum is in that segment's canonical frame; at the segment's end it is rotated
-// by R(-(t - p_s)) -- RestorePhase R(+p_s) followed by the inverse output RoPE
-// R(-t) (Alg. 2, eq:offonline) -- and added to the row's total, which is
-// written after the latent dims of the partial (or of the bf16 head output).
-// ----------------------------------------------------------------------------
-template <int DC, int DR>
-__global__ __launch_bounds__(256, 1) void attend_vrope_kernel(AttendArgs a) {
-  using C = Cfg<DC, DR>;
-  static_assert(DR == 64, "rotation pairs (j, j + 32) sit in one lane of the two RoPE output blocks");
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2 * C::TILE_BYTES];
-
-  unsigned char MLA_LDS* L = (unsigned char MLA_LDS*)lds;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int half = lane >> 5, l32 = lane & 31;
-
-  const int item_id = xcd_item_id(blockIdx.x);
-  if (item_id >= item_count(a)) return;
-  const ItemView v = item_view<C>(a, item_id, wave, l32);
-  const SegInfo* segs = v.segs;
-  const int32_t* rank_seg = v.rank_seg;
-  const WorkItem& it = v.it;
-  const ChunkInfo& chk = v.chk;
-  const bool valid = v.valid, active = v.active;
-  const int64_t slot = v.slot, t_pos = v.t_pos;
-  const uint16_t* qsrc = v.qsrc;
-  const double* theta_rev = v.theta_rev;
-  const int64_t pidx = a.out_direct != nullptr ? slot : a.part_ptr[slot] + it.chunk;
-  // this head-row's log2-sum-exp over the chunk (from the latent pass)
-  const float lse2 = valid ? a.part_lse[pidx] * 1.4426950408889634f : 0.f;
-
-  bf16x8 qf[C::KS];
-#pragma unroll
-  for (int ks = 0; ks < C::KS; ++ks) {
-    qf[ks] = *(const bf16x8*)(qsrc + ks * 16 + half * 8);
-    if (!valid) qf[ks] = bf16x8{};
-  }
-
-  int abase[4];
-#pragma unroll
-  for (int s4 = 0; s4 < 4; ++s4)
-    abase[s4] = (l32 >> 3) * C::KB8 + (l32 & 7) * 128 + (((2 * s4 + half) ^ rotl3(l32 & 7)) * 16);
-  const int q4 = lane >> 4, rr = (lane >> 2) & 3, cb = lane & 3;
-  const int vkey = (q4 >> 1) * 4 + rr;
-  int vb[2][2];
-#pragma unroll
-  for (int dp = 0; dp < 2; ++dp)
-#pragma unroll
-    for (int kq = 0; kq < 2; ++kq)
-      vb[dp][kq] = vkey * 128 + (((dp * 4 + (q4 & 1) * 2 + (cb >> 1)) ^ rotl3(vkey)) * 16) + (cb & 1) * 8 +
-                   kq * 4 * C::KB8;
-  const int lkey = lane >> 3;
-  const int lchunk_full = (lane & 7) ^ rotl3(lkey);
-  const int lchunk_part = (lane & 7) < (C::CH - C::CGF * 8) ? (lane & 7) : 0;
-
-  auto issue = [&](unsigned char MLA_LDS* dbuf, const SegInfo& sg, int64_t n_keys, int64_t tile) {
-    issue_tile<C>(a.kv, sg, n_keys, tile, dbuf, wave, lkey, lchunk_full, lchunk_part);
-  };
-
-  int c_rank = chk.first_rank;
-  SegInfo cs = segs[rank_seg[c_rank]];
-  int64_t c_tile = 0;
-  int n_rank = c_rank;
-  SegInfo ns = cs;
-  int64_t n_keys = seg_keys(v, cs, rank_seg[c_rank] == it.seg);
-  int64_t n_ntiles = (n_keys + C::BK - 1) / C::BK;
-  int64_t n_tile = 0;
-  int lim = 0x7fffffff, wave_lim = 0x7fffffff;
-
-  auto relocate = [&](const SegInfo& sg) {
-    lim = relocate_query<C, DC, DR>(qf, v, sg, half);
-    wave_lim = wave_min_i(lim);
-  };
-  auto advance = [&]() -> bool {
-    if (n_tile + 1 < n_ntiles) {
-      ++n_tile;
-      return true;
-    }
-    if (n_rank >= chk.last_rank) return false;
-    ++n_rank;
-    const int sidx = rank_seg[n_rank];
-    ns = segs[sidx];
-    n_keys = seg_keys(v, ns, sidx == it.seg);
-    n_ntiles = (n_keys + C::BK - 1) / C::BK;
-    n_tile = 0;
-    return true;
-  };
-
-  // rope output: this segment's sum (canonical frame) and the row's total
-  f32x16 racc[2], rtot[2];
-#pragma unroll
-  for (int d = 0; d < 2; ++d)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      racc[d][e] = 0.f;
-      rtot[d][e] = 0.f;
-    }
-  // lane holds rope dims half*4 + 8i + j (reg 4i + j) of block 0 and their pair
-  // partners (+32) in block 1: rotate the pairs by R(-(t - p_s)) into the total
-  auto close_segment = [&](const SegInfo& sg) {
-    const double dd = (double)(t_pos - sg.req_offset);
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int k = half * 4 + (e >> 2) * 8 + (e & 3);
-      const double rev = dd * theta_rev[k];
-      const float r = (float)(rev - rint(rev));
-      const float sn = __builtin_amdgcn_sinf(r), cn = __builtin_amdgcn_cosf(r);
-      const float x = racc[0][e], y = racc[1][e];
-      rtot[0][e] += x * cn + y * sn;
-      rtot[1][e] += y * cn - x * sn;
-      racc[0][e] = 0.f;
-      racc[1][e] = 0.f;
-    }
-  };
-
-  const float sl2 = a.scale_log2;
-  relocate(cs);
-  issue(L, cs, n_keys, 0);
-  int cur = 0;
-  for (;;) {
-    tile_barrier();
-    const bool more = advance();
-    if (more) issue(L + (C::TILE_BYTES - cur), ns, n_keys, n_tile);
-    const unsigned char MLA_LDS* buf = L + cur;
-    if (active) {
-      f32x16 s[2];
-      auto kfrag = [&](int kt, int ks) -> bf16x8 {
-        return *(const bf16x8 MLA_LDS*)(buf + abase[ks & 3] + (ks >> 2) * 1024 + kt * 4 * C::KB8);
-      };
-      bf16x8 ka[3][2];
-      ka[0][0] = kfrag(0, 0);
-      ka[0][1] = kfrag(1, 0);
-      ka[1][0] = kfrag(0, 1);
-      ka[1][1] = kfrag(1, 1);
-      // compiler-visible MFMAs here (the registers are not full): the compiler
-      // keeps the operand and result wait states itself
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        s[0][e] = 0.f;
-        s[1][e] = 0.f;
-      }
-#pragma unroll
-      for (int ks = 0; ks < C::KS; ++ks) {
-        if (ks + 2 < C::KS) {
-          ka[(ks + 2) % 3][0] = kfrag(0, ks + 2);
-          ka[(ks + 2) % 3][1] = kfrag(1, ks + 2);
-        }
-        // the scheduling barriers keep the K reads two steps ahead of their MFMAs
-        __builtin_amdgcn_sched_barrier(0);
-        s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks % 3][0], qf[ks], s[0], 0, 0, 0);
-        s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks % 3][1], qf[ks], s[1], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      const int tk0 = (int)(c_tile * C::BK);
-      if (tk0 + C::BK - 1 > wave_lim) {
-        const int rel = lim - tk0 - ((int)(__lane_id() >> 5) << 2);
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = (e >> 2) * 8 + (e & 3);
-          if (key > rel) s[0][e] = -INFINITY;
-          if (key + 32 > rel) s[1][e] = -INFINITY;
-        }
-      }
-      bf16x8 pf[C::PS];
-      const float nl = -lse2;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e)
-          pf[kt * 2 + (e >> 3)][e & 7] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][e], sl2, nl));
-      // O_r^T += K_r^T P^T: output blocks DC/32 and DC/32 + 1 of the transposing V reads
-      bf16x8 vt[C::PS][2];
-#pragma unroll
-      for (int s2 = 0; s2 < C::PS; ++s2)
-#pragma unroll
-        for (int dd = 0; dd < 2; ++dd) {
-          const int d = C::OB + dd;
-          const int off = vb[d & 1][s2 >> 1] + (d >> 1) * 1024 + (s2 & 1) * 2 * C::KB8;
-          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((MLA_LDS bf16x4*)(buf + off));
-          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((MLA_LDS bf16x4*)(buf + off + C::KB8));
-          vt[s2][dd] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        }
-#pragma unroll
-      for (int s2 = 0; s2 < C::PS; ++s2)
-#pragma unroll
-        for (int dd = 0; dd < 2; ++dd)
-          racc[dd] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt[s2][dd], pf[s2], racc[dd], 0, 0, 0);
-    }
-    if (!more) break;
-    if (n_rank != c_rank) {
-      close_segment(cs);
-      c_rank = n_rank;
-      cs = ns;
-      relocate(cs);
-    }
-    c_tile = n_tile;
-    cur = C::TILE_BYTES - cur;
-  }
-  tile_barrier();
-  close_segment(cs);
-  if (!valid) return;
-  if (a.out_direct != nullptr && a.out_direct_bf16) {
-    uint16_t* ob = (uint16_t*)a.out_direct + slot * a.dv + DC;
-#pragma unroll
-    for (int d = 0; d < 2; ++d)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        *(u32x2*)(ob + d * 32 + half * 4 + 8 * i) = u32x2{pack_bf16x2(rtot[d][4 * i], rtot[d][4 * i + 1]),
-                                                          pack_bf16x2(rtot[d][4 * i + 2], rtot[d][4 * i + 3])};
-    return;
-  }
-  float* dst = (a.out_direct != nullptr ? (float*)a.out_direct : a.part_o) + pidx * a.dv + DC;
-#pragma unroll
-  for (int d = 0; d < 2; ++d)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      f32x4 v = {rtot[d][4 * i], rtot[d][4 * i + 1], rtot[d][4 * i + 2], rtot[d][4 * i + 3]};
-      *(f32x4*)(dst + d * 32 + half * 4 + 8 * i) = v;
-    }
-}
 
 // ----------------------------------------------------------------------------
 // device half of the plan
@@ -930,19 +880,18 @@ hipError_t launch_plan(const AttendArgs& a, hipStream_t s) {
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
   if (a.n_items == 0) return hipSuccess;
   const unsigned grid = (unsigned)(((int64_t)a.n_items + 255) / 256 * 256);
-  if (a.d_latent == 512 && a.d_rope == 64)
-    attend_kernel<512, 64><<<dim3(grid), dim3(256), 0, s>>>(a);
-  else if (a.d_latent == 64 && a.d_rope == 16)
-    attend_kernel<64, 16><<<dim3(grid), dim3(256), 0, s>>>(a);
-  else
+  const bool rot = a.dv != a.d_latent;   // rotary value: the RoPE dims too (needs a.rot)
+  if (rot && (a.d_latent != 512 || a.d_rope != 64 || a.rot == nullptr)) return hipErrorInvalidValue;
+  if (a.d_latent == 512 && a.d_rope == 64) {
+    if (rot)
+      attend_kernel<512, 64, true><<<dim3(grid), dim3(256), 0, s>>>(a);
+    else
+      attend_kernel<512, 64, false><<<dim3(grid), dim3(256), 0, s>>>(a);
+  } else if (a.d_latent == 64 && a.d_rope == 16) {
+    attend_kernel<64, 16, false><<<dim3(grid), dim3(256), 0, s>>>(a);
+  } else {
     return hipErrorInvalidValue;
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.dv == a.d_latent) return e;
-  // rotary value: the RoPE dims of the head outputs, after the latent pass (its lse)
-  if (a.d_latent == 512 && a.d_rope == 64)
-    attend_vrope_kernel<512, 64><<<dim3(grid), dim3(256), 0, s>>>(a);
-  else
-    return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -74,7 +74,9 @@ struct PlanHeader {
   int64_t off_prot_seg;    // int32[n_prot]: segment of each protected row
   int64_t off_cum_local;   // int64[n_prot + 1]: local-slot partials before row a
   int64_t off_theta;       // double[d_r/2]: base^(-2j/d_r) / (2 pi), RoPE frequency in revolutions
-  int64_t total_bytes;
+  int64_t total_bytes;     // bytes of the image (the part uploaded)
+  int64_t off_rot;         // rotary value: f32[n_items * 128 * 128] accumulators after the image, else -1
+  int64_t ws_bytes;        // image and accumulators
 };
 
 // Device-built plan (the protected set comes from device memory): the work
@@ -107,8 +109,7 @@ struct AttendArgs {
   const void* q_glob;
   const void* q_loc;
   float* part_o;             // [n_parts, dv] normalized partials (unused with out_direct)
-  float* part_lse;           // [n_parts] natural-log lse; with out_direct [slots] (may be NULL then,
-                             // except with a rotary value, whose second pass reads it)
+  float* part_lse;           // [n_parts] natural-log lse; with out_direct [slots] (may be NULL then)
   int64_t* part_ptr;         // [n_slots + 1] CSR offsets of each slot's partials
   int32_t* part_seg;         // [n_parts, 2] or NULL
   uint8_t* row_src;          // [n_rows] or NULL
@@ -142,6 +143,7 @@ struct AttendArgs {
   void* out_direct;          // if set: one chunk per slot, the normalized O written here [slots, dv]
                              // (part_o unused)
   int32_t out_direct_bf16;   // element type of out_direct: 1 bf16, 0 f32
+  float* rot;                // rotary value: [slots (out_direct) or n_parts, 128] f32 accumulators
 };
 
 hipError_t launch_plan(const AttendArgs& a, hipStream_t s);
