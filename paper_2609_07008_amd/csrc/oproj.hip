@@ -3,11 +3,14 @@
 // z = z_online + z_off on unprotected rows, z = z_online on protected rows).
 //
 // Two bf16 MFMA GEMM passes per projection group pg, both on the caller's stream:
-//   pass L: rows a of the protected set, K = the Local heads of pg's groups;
-//           the result is written straight into z[prot_rows[a]].
 //   pass G: every row, K = the Global heads of pg's groups; the epilogue adds
-//           z_off[r] on unprotected rows and the pass-L value already in z[r]
-//           on protected rows, so z_off is never read for protected rows.
+//           z_off[r] on unprotected rows and nothing on protected rows, so
+//           z_off is never read for protected rows (the replace);
+//   pass L: rows a of the protected set, K = the Local heads of pg's groups;
+//           the result is added to the pass-G value in z[prot_rows[a]] (or, for
+//           the offline producer, which runs pass L alone, written there).
+// An epilogue loads the values it adds a 32-row block at a time, before the
+// block's first store, so that their latencies overlap.
 // Each head's weight rows are a d_c-row block of w_o[pg]; a K tile of 64 never
 // straddles two heads, so the B operand is gathered per tile by head.  The MFMAs
 // compute the transposed tile (W^T O^T), so that each lane holds one output row
@@ -27,7 +30,7 @@ constexpr int OP_ALD = OP_BK + 8;     // padded A row (bf16): 144 B, conflict-fr
 template <int PASS, int BM, int BN, int WM, int WN>   // PASS 0 = Local over protected rows, 1 = Global
 // at most 128 registers per wave, so that two workgroups of 8 waves share a CU
 __global__ __launch_bounds__(WM * WN * 64) __attribute__((amdgpu_waves_per_eu(4)))
-void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
+void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles, int local_add) {
   constexpr int NT = WM * WN * 64;
   // padded B row: 2*BLD = 64 mod 256 bytes, so the four k-rows that each half-wave
   // of a transposing read touches land on disjoint 16-bank groups (all 64 banks)
@@ -46,7 +49,7 @@ void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
   __shared__ int row_flag[OP_BM];
   __shared__ int row_out[OP_BM];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hpg = a.n_heads / a.n_groups;
   const int gpp = a.n_groups / a.n_pg;              // output groups per projection group
   const int cw = a.d_model / a.n_pg;                // channels per projection group
@@ -228,8 +231,57 @@ void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
   float MLA_LDS* stage = (float MLA_LDS*)As + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) * (32 * SLD);
   const uint16_t* zoff = (const uint16_t*)a.z_off;
   const int prow = elane >> 3, pc4 = (elane & 7) * 4;   // read-back: row prow + 8p, channels pc4 .. +3
+  // the values this block adds: pass G, bf16 z_off of the unprotected rows (none
+  // on protected rows); pass L after pass G, the row's z (f32 bits, or bf16)
+  const bool add_any = PASS == 1 || local_add != 0;
 #pragma unroll
-  for (int mi = 0; mi < MI; ++mi)
+  for (int mi = 0; mi < MI; ++mi) {
+    u32x4 addv[NI][4];
+    f32x4 addf[NI][4];
+    if (add_any) {
+      // every lane loads (element 0 where nothing is added) and the unused
+      // values are zeroed after: no branch around the loads, so each later wait
+      // counts exactly the loads still ahead of it
+      auto add_off = [&](int ni, int p, bool& use) -> int64_t {
+        const int n = n0 + wn * TN + ni * 32 + pc4;
+        const int r = wm * TM + mi * 32 + p * 8 + prow;
+        const int64_t orow = m0 + r < M && n < cw ? (int64_t)row_out[r] : -1;
+        use = orow >= 0 && (PASS == 0 || !row_flag[r]);
+        return use ? orow * a.d_model + (int64_t)pg * cw + n : 0;
+      };
+      if (PASS == 1 || a.z_bf16) {
+        const uint16_t* src = PASS == 1 ? zoff : (const uint16_t*)a.z;
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+          for (int p = 0; p < 4; ++p) {
+            bool use;
+            const u32x2 zz = *(const u32x2*)(src + add_off(ni, p, use));
+            addv[ni][p] = use ? u32x4{zz[0], zz[1], 0u, 0u} : u32x4{0u, 0u, 0u, 0u};
+          }
+      } else {
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+          for (int p = 0; p < 4; ++p) {
+            bool use;
+            const u32x4 w = *(const u32x4*)(a.z + add_off(ni, p, use));
+            addv[ni][p] = use ? w : u32x4{0u, 0u, 0u, 0u};
+          }
+      }
+      // widened to f32 here, so that the block's one wait for its loads comes
+      // before any of its stores (later waits would count those stores too)
+#pragma unroll
+      for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const u32x4 w = addv[ni][p];
+          addf[ni][p] = PASS == 1 || a.z_bf16
+                            ? f32x4{bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])}
+                            : f32x4{__uint_as_float(w[0]), __uint_as_float(w[1]), __uint_as_float(w[2]),
+                                    __uint_as_float(w[3])};
+        }
+    }
 #pragma unroll
     for (int ni = 0; ni < NI; ++ni) {
 #pragma unroll
@@ -244,29 +296,16 @@ void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles) {
         const int r = wm * TM + mi * 32 + rr;       // tile row
         if (m0 + r >= M || n >= cw) continue;
         const int64_t orow = row_out[r];
-        if (PASS == 0 && orow < 0) continue;
+        if (orow < 0) continue;
         const int64_t off = orow * a.d_model + (int64_t)pg * cw + n;
-        if (PASS == 1) {
-          if (row_flag[r]) {
-            if (hpg > 1) {   // the Local pass wrote this row first
-              if (a.z_bf16) {
-                const u32x2 zl = *(const u32x2*)((const uint16_t*)a.z + off);
-                v += f32x4{bf16_lo(zl[0]), bf16_hi(zl[0]), bf16_lo(zl[1]), bf16_hi(zl[1])};
-              } else {
-                v += *(const f32x4*)(a.z + off);
-              }
-            }
-          } else {
-            const u32x2 zz = *(const u32x2*)(zoff + off);
-            v += f32x4{bf16_lo(zz[0]), bf16_hi(zz[0]), bf16_lo(zz[1]), bf16_hi(zz[1])};
-          }
-        }
+        if (add_any) v += addf[ni][p];
         if (a.z_bf16)
           *(u32x2*)((uint16_t*)a.z + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
         else
           *(f32x4*)(a.z + off) = v;
       }
     }
+  }
 }
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(u32x4* p, int64_t n16) {
@@ -297,24 +336,25 @@ int64_t oproj_workgroups(int64_t M, int d_model, int n_pg) {
 }
 
 template <int PASS>
-hipError_t launch_pass(const OprojArgs& a, int64_t M, hipStream_t s) {
+hipError_t launch_pass(const OprojArgs& a, int64_t M, int local_add, hipStream_t s) {
   constexpr int BM = kOpBM, BN = kOpBN, WM = kOpWM, WN = kOpWN;
   const int cw = a.d_model / a.n_pg;
   const int n_tiles = (cw + BN - 1) / BN;
   const int m_tiles = (int)((M + BM - 1) / BM);
   const int total = m_tiles * n_tiles * a.n_pg;
   oproj_kernel<PASS, BM, BN, WM, WN><<<dim3((unsigned)(8 * ((total + 7) / 8))), dim3(WM * WN * 64), 0, s>>>(
-      a, m_tiles, n_tiles);
+      a, m_tiles, n_tiles, local_add);
   return hipGetLastError();
 }
 
 hipError_t launch_oproj(const OprojArgs& a, int passes, hipStream_t s) {
   const int hpg = a.n_heads / a.n_groups;
-  if ((passes & 1) && a.n_prot > 0 && hpg > 1) {
-    const hipError_t e = launch_pass<0>(a, a.n_prot, s);
+  if ((passes & 2) && a.n_rows > 0) {
+    const hipError_t e = launch_pass<1>(a, a.n_rows, 0, s);
     if (e != hipSuccess) return e;
   }
-  if ((passes & 2) && a.n_rows > 0) return launch_pass<1>(a, a.n_rows, s);
+  // after pass G the Local values add to z; alone (the producer) they are written
+  if ((passes & 1) && a.n_prot > 0 && hpg > 1) return launch_pass<0>(a, a.n_prot, (passes & 2) ? 1 : 0, s);
   return hipSuccess;
 }
 
