@@ -49,11 +49,13 @@ def artifact_bf16(wl):
     return round_bf16(M.artifact(wl).astype(np.float32)).astype(np.float64)
 
 
-def compare_rows(wl, st, rows, z_off, kv=None, keys=None, lse_abs_tol=ABS_TOL):
+def compare_rows(wl, st, rows, z_off, kv=None, keys=None, lse_abs_tol=ABS_TOL, z_abs_tol=ABS_TOL):
     """Oracle vs GPU on storage rows `rows`: O and lse of every online head, z_online and z.
     `lse_abs_tol` widens the absolute bound on lse alone, for planted scores far
     above the workload's range: the kernel rounds the relocated query to bf16,
-    so its score error (and the lse error) grows with the score itself."""
+    so its score error (and the lse error) grows with the score itself.
+    `z_abs_tol` (a scalar, or one bound per sorted row and channel) does the same
+    for z, whose input is the bf16-rounded head outputs (see rounded_o_bound)."""
     g = wl.geom
     rows = np.asarray(sorted(set(int(r) for r in rows)), dtype=np.int64)
     if isinstance(z_off, np.ndarray):
@@ -87,13 +89,31 @@ def compare_rows(wl, st, rows, z_off, kv=None, keys=None, lse_abs_tol=ABS_TOL):
     if z_bf16:
         # z stored in bf16: each element carries up to two roundings of 2^-9 |z|
         # (a protected row's Local sum, then z), which z - z_off inherits
-        allow = ABS_TOL + 2.0 ** -8 * np.abs(ref.z)
+        allow = z_abs_tol + 2.0 ** -8 * np.abs(ref.z)
         assert np.all(np.abs(z - zoff_rows - ref.z_online) <= allow), "z_online (bf16 z)"
-        check("z", z, ref.z, bf16_out=True)
+        check("z", z, ref.z, abs_tol=z_abs_tol, bf16_out=True)
     else:
-        check("z_online", z - zoff_rows, ref.z_online)
-        check("z", z, ref.z)
+        check("z_online", z - zoff_rows, ref.z_online, abs_tol=z_abs_tol)
+        check("z", z, ref.z, abs_tol=z_abs_tol)
     return ref
+
+
+def rounded_o_bound(wl, rows, kv=None, keys=None):
+    """Per sorted row and channel, the most that rounding the row's head outputs
+    to bf16 (half an ulp, 2^-8 of each value) can move z: 2^-8 sum_h |o_h| |W_h|,
+    with the oracle's o.  Added to the absolute z bound where planted scores make
+    the head outputs large."""
+    g = wl.geom
+    rows = np.asarray(sorted(set(int(r) for r in rows)), dtype=np.int64)
+    zr = wl.z_off(rows=rows)
+    ref = M.reference_rows(wl, rows, z_off={int(r): zr[i] for i, r in enumerate(rows)}, kv=kv, keys=keys)
+    blocks = np.abs(M.dense_blocks(wl.w_o(), g.n_heads, g.d_v, g.d_model))
+    out = np.zeros((rows.shape[0], g.d_model))
+    for i in range(rows.shape[0]):
+        out[i] = M.project(np.abs(ref.o_glob[i]), wl.global_head_ids(), blocks)
+        if i in ref.o_loc:
+            out[i] += M.project(np.abs(ref.o_loc[i]).reshape(-1, g.d_v), wl.local_head_ids().reshape(-1), blocks)
+    return 2.0 ** -8 * out
 
 
 def check_bookkeeping(wl, st, split_keys, full_part_seg=True):
