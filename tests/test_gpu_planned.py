@@ -110,6 +110,25 @@ def test_planned_equals_host_path(name, split, cap):
     assert torch_equal(st.out_o[n_slots:], None)     # rows past the slots of |A| stay untouched
 
 
+@pytest.mark.parametrize("name", ["ragged", "dense_proj", "wide_groups"])
+@pytest.mark.parametrize("split", [0, 100, 10 ** 9])
+def test_planned_equals_host_path_rotary_value(name, split):
+    """The same equality with a rotary value: the RoPE output sums of every work
+    item live in the workspace (a different item layout and place on each
+    path), and each head-row's sums, rotations and normalization are still
+    bit-identical."""
+    wl = make_custom(d_c=512, d_r=64, seed=310 + sorted(CUSTOM).index(name), fp32=False, value_rope=True,
+                     **CUSTOM[name])
+    assert wl.geom.d_v == 576
+    split = min(split, wl.n_rows)
+    host, inputs = run(wl, split)
+    st = _planned(wl, split, wl.n_prot, inputs)
+    n_slots = host.n_slots
+    assert torch_equal(st.out_o[:n_slots], host.out_o)
+    assert torch_equal(st.out_lse[:n_slots], host.out_lse)
+    assert torch_equal(st.z, host.z)
+
+
 def torch_equal(a, b):
     import torch
     if b is None:                                     # never written: still the 0xFF fill
