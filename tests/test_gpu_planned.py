@@ -275,14 +275,17 @@ def test_device_list_rejected(case):
     assert torch_equal(st.out_o[: host.n_slots], host.out_o)
 
 
-def test_planned_graph_replay_follows_device_set():
+@pytest.mark.parametrize("value_rope", [False, True], ids=["latent_value", "rotary_value"])
+def test_planned_graph_replay_follows_device_set(value_rope):
     """attend + o-proj captured once; each replay reads the protected set that
     the device buffers hold at that time, so a new set (another layer's) needs
-    no new capture.  Every replay equals the eager call on the same set."""
+    no new capture.  Every replay equals the eager call on the same set.  With a
+    rotary value the replays also reuse the RoPE output sums in the workspace,
+    which each item clears itself."""
     import torch
     from paper_2609_07008_amd import device_inputs, step
     kw = dict(doc_lens=[70, 90, 66], req_perm=[2, 0, 1], tq=12, H=16, G=2, d_c=512, d_r=64, d_model=256,
-              fp32=False, seed=73)
+              fp32=False, seed=73, value_rope=value_rope)
     wl_a = make_custom(prot_frac=0.2, **kw)
     rng = np.random.default_rng(74)
     n = wl_a.n_rows
