@@ -729,7 +729,9 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   // ---- epilogue: combine the two lane halves' row sums, store normalized partial and lse ----
   float lx, ly;
   lane_halves(l_run, lx, ly);
-  if (!valid) return;
+  // bf16 head outputs go through LDS, where every lane of the wave helps
+  const bool staged = a.out_direct != nullptr && a.out_direct_bf16;
+  if (!valid && !staged) return;
   const float l_tot = lx + ly;
   const float inv = 1.f / l_tot;
   // rotary value: the last segment's sum into the row's total, normalized
@@ -750,15 +752,37 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   if (a.out_direct != nullptr) {
     // one chunk per slot (the merge done here by online rescaling, or the
     // offline producer): the head output itself, and its lse when asked for
-    if (a.part_lse != nullptr && half == 0) a.part_lse[slot] = (m_run + __log2f(l_tot)) * 0.6931471805599453f;
+    if (valid && a.part_lse != nullptr && half == 0)
+      a.part_lse[slot] = (m_run + __log2f(l_tot)) * 0.6931471805599453f;
     if (a.out_direct_bf16) {
-      uint16_t* ob = (uint16_t*)a.out_direct + slot * a.dv;
+      // The wave's 32 head-rows own consecutive slots.  Their latent dims go
+      // through the wave's part of the tile buffers (idle since the last tile
+      // barrier): written in the accumulator layout (lane: row l32, dims half*4 +
+      // 8i of each block), read back row-contiguous (lane: 8 consecutive dims;
+      // DC/8 lanes a row), so each global store writes whole rows (one contiguous
+      // kilobyte for d_c = 512).  Rows are padded by 8 bytes (1032 for d_c = 512),
+      // so the 32 lanes of a half-wave write 64 distinct banks.
+      constexpr int SROW = DC + 4;   // staged row, bf16 elements
+      constexpr int LPR = DC / 8;    // lanes per row on the way out
+      static_assert(4 * 32 * SROW * 2 <= 2 * C::TILE_BYTES && 64 % LPR == 0, "staging fits the tile buffers");
+      uint16_t MLA_LDS* srow = (uint16_t MLA_LDS*)L + wave * 32 * SROW;
 #pragma unroll
       for (int d = 0; d < C::OB; ++d)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          *(u32x2*)(ob + d * 32 + half * 4 + 8 * i) = u32x2{pack_bf16x2(o[d][4 * i] * inv, o[d][4 * i + 1] * inv),
-                                                            pack_bf16x2(o[d][4 * i + 2] * inv, o[d][4 * i + 3] * inv)};
+          *(u32x2 MLA_LDS*)(srow + l32 * SROW + d * 32 + half * 4 + 8 * i) =
+              u32x2{pack_bf16x2(o[d][4 * i] * inv, o[d][4 * i + 1] * inv),
+                    pack_bf16x2(o[d][4 * i + 2] * inv, o[d][4 * i + 3] * inv)};
+      const int nrow = it.count - wave * 32 < 32 ? it.count - wave * 32 : 32;   // valid rows of the wave
+      const int64_t slot0 = (it.kind == 0 ? 0 : a.local_slot_base) + it.hr_begin + wave * 32;
+      uint16_t* ob0 = (uint16_t*)a.out_direct + slot0 * a.dv;
+      for (int r0 = 0; r0 < nrow; r0 += 64 / LPR) {
+        const int r = r0 + lane / LPR, cl = lane % LPR;
+        if (r < nrow)
+          *(u32x4*)(ob0 + (int64_t)r * a.dv + cl * 8) = *(const u32x4 MLA_LDS*)(srow + r * SROW + cl * 8);
+      }
+      if (!valid) return;
+      uint16_t* ob = (uint16_t*)a.out_direct + slot * a.dv;
       if (ROT)
 #pragma unroll
         for (int d = 0; d < 2; ++d)
