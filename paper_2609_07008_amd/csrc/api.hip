@@ -997,6 +997,7 @@ struct OfflineLayout {
   Plan plan;
   std::vector<int32_t> rows;   // identity row list: every row computes its Local heads
   size_t off_o = 0;            // bf16 head outputs [N, G, hpg-1, dv]
+  size_t off_wt = 0;           // W_{a,L}^T per projection group [n_pg, d_model/n_pg, K_L] bf16
   size_t total = 0;
 };
 
@@ -1014,7 +1015,9 @@ mla_status offline_layout(const mla_geom* geom, const mla_segment* segs, int32_t
   const size_t n_out = (size_t)N * geom->n_groups * (hpg - 1);
   const size_t o_bytes = n_out * head_dv(geom) * 2;
   L->off_o = align_up((size_t)L->plan.hdr.ws_bytes, 256);
-  L->total = L->off_o + align_up(o_bytes, 256);
+  L->off_wt = L->off_o + align_up(o_bytes, 256);
+  const size_t kl = (size_t)(geom->n_groups / geom->n_proj_groups) * (hpg - 1) * head_dv(geom);
+  L->total = L->off_wt + align_up((size_t)geom->d_model * kl * 2, 256);
   return MLA_OK;
 }
 
@@ -1062,6 +1065,12 @@ mla_status mla_offline_produce(const mla_geom* geom, const mla_segment* segs, in
   if (mla::oproj_workgroups(N, geom->d_model, geom->n_proj_groups) > INT32_MAX)
     return fail(MLA_ERR_UNSUPPORTED, "%lld rows x d_model %d is more o-proj tiles than one launch takes",
                 (long long)N, geom->d_model);
+  {
+    // the Local projection's direct loads address a wave's 64 rows with 32-bit offsets
+    const int64_t ldz = (int64_t)geom->n_groups * (hpg - 1) * head_dv(geom);
+    if (64 * ldz * 2 >= ((int64_t)1 << 32))
+      return fail(MLA_ERR_UNSUPPORTED, "Local head outputs of %lld elements a row", (long long)ldz);
+  }
   if ((st = upload_plan(L.plan, workspace, s)) != MLA_OK) return st;
 
   unsigned char* ws = reinterpret_cast<unsigned char*>(workspace);
@@ -1100,8 +1109,30 @@ mla_status mla_offline_produce(const mla_geom* geom, const mla_segment* segs, in
   op.n_pg = geom->n_proj_groups;
   op.z_bf16 = out_dtype == MLA_BF16 ? 1 : 0;
   for (int g = 0; g < geom->n_groups; ++g) op.glob_head[g] = glob_head[g];
-  e = mla::launch_oproj(op, 1, s);
-  if (e != hipSuccess) return hip_fail(e, "o-proj kernel");
+  // z_off = W_{a,L} O_L per projection group as one batched K-contiguous GEMM on
+  // the shared-W_b kernel: O_L's columns of the group against its Local weights,
+  // transposed once per call into the workspace
+  uint16_t* wt = reinterpret_cast<uint16_t*>(ws + L.off_wt);
+  if ((e = mla::launch_local_wt(op, wt, s)) != hipSuccess) return hip_fail(e, "weight transpose kernel");
+  const int gpp = geom->n_groups / geom->n_proj_groups;
+  const int dv = head_dv(geom);
+  const int cw = geom->d_model / geom->n_proj_groups;
+  mla::WbArgs g{};
+  g.z = reinterpret_cast<const uint16_t*>(ws + L.off_o);
+  g.w_b = wt;
+  g.y = z_off;
+  g.n_rows = N;
+  g.d_in = gpp * (hpg - 1) * dv;
+  g.d_out = cw;
+  g.y_bf16 = out_dtype == MLA_BF16 ? 1 : 0;
+  g.batch = geom->n_proj_groups;
+  g.ldz = (int64_t)geom->n_groups * (hpg - 1) * dv;
+  g.ldw = g.d_in;
+  g.ldy = geom->d_model;
+  g.z_batch = (int64_t)gpp * (hpg - 1) * dv;
+  g.w_batch = (int64_t)cw * g.d_in;
+  g.y_batch = cw;
+  if ((e = mla::launch_wb(g, s)) != hipSuccess) return hip_fail(e, "Local projection kernel");
   return MLA_OK;
 }
 
@@ -1358,6 +1389,9 @@ mla_status mla_shared_wb(int64_t n_rows, int32_t d_in, int32_t d_out, const void
   a.d_in = d_in;
   a.d_out = d_out;
   a.y_bf16 = out_dtype == MLA_BF16 ? 1 : 0;
+  a.batch = 1;
+  a.ldz = a.ldw = d_in;
+  a.ldy = d_out;
   const hipError_t e = mla::launch_wb(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "shared W_b kernel");
   return MLA_OK;

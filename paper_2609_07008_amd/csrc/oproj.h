@@ -29,5 +29,8 @@ hipError_t launch_oproj(const OprojArgs& a, int passes, hipStream_t s);
 // grid size of one o-proj pass over M rows (the kernel indexes its tiles with int)
 int64_t oproj_workgroups(int64_t M, int d_model, int n_pg);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+// the producer's Local weights transposed: wt [n_pg, d_model/n_pg, K_L] bf16, K_L =
+// (G/n_pg)(hpg-1)d_v (a.d_latent is the head output width)
+hipError_t launch_local_wt(const OprojArgs& a, uint16_t* wt, hipStream_t s);
 
 }  // namespace mla

@@ -308,6 +308,56 @@ void oproj_kernel(OprojArgs a, int m_tiles, int n_tiles, int local_add) {
   }
 }
 
+// W_{a,L}^T of each projection group, for the producer's Local projection as a
+// plain K-contiguous GEMM: wt[pg][n][k] = w_o[pg][row(k)][n], k running over the
+// Local heads of pg's groups in the order of the head outputs' columns (ascending
+// head index, the group's Global head skipped).  64 x 64 tiles through LDS, so
+// that both the reads (along n) and the writes (along k) are row-contiguous.
+__global__ __launch_bounds__(256) void local_wt_kernel(OprojArgs a, uint16_t* wt, int n_ktiles, int n_ntiles) {
+  __shared__ uint16_t tile[64][65];
+  const int hpg = a.n_heads / a.n_groups, gpp = a.n_groups / a.n_pg;
+  const int cw = a.d_model / a.n_pg, DC = a.d_latent;
+  const int heads_pp = a.n_heads / a.n_pg;
+  const int64_t KL = (int64_t)gpp * (hpg - 1) * DC;
+  int b = blockIdx.x;
+  const int kt = b % n_ktiles;
+  b /= n_ktiles;
+  const int nt = b % n_ntiles;
+  const int pg = b / n_ntiles;
+  const uint16_t* W = (const uint16_t*)a.w_o + (int64_t)pg * heads_pp * DC * cw;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int r = ty; r < 64; r += 4) {   // read: tile row r = k, column tx = n
+    const int64_t k = (int64_t)kt * 64 + r;
+    const int n = nt * 64 + tx;
+    uint16_t v = 0;
+    if (k < KL && n < cw) {
+      const int kb = (int)(k / DC), d = (int)(k - (int64_t)kb * DC);
+      const int gl = kb / (hpg - 1), j = kb - gl * (hpg - 1);
+      const int gh = a.glob_head[pg * gpp + gl];
+      const int hl = gl * hpg + (j < gh ? j : j + 1);
+      v = W[((int64_t)hl * DC + d) * cw + n];
+    }
+    tile[r][tx] = v;
+  }
+  __syncthreads();
+  for (int r = ty; r < 64; r += 4) {   // write: row n, column k
+    const int n = nt * 64 + r;
+    const int64_t k = (int64_t)kt * 64 + tx;
+    if (n < cw && k < KL) wt[((int64_t)pg * cw + n) * KL + k] = tile[tx][r];
+  }
+}
+
+hipError_t launch_local_wt(const OprojArgs& a, uint16_t* wt, hipStream_t s) {
+  const int hpg = a.n_heads / a.n_groups, gpp = a.n_groups / a.n_pg;
+  const int64_t KL = (int64_t)gpp * (hpg - 1) * a.d_latent;
+  const int cw = a.d_model / a.n_pg;
+  const int n_ktiles = (int)((KL + 63) / 64), n_ntiles = (cw + 63) / 64;
+  const int64_t blocks = (int64_t)n_ktiles * n_ntiles * a.n_pg;
+  if (blocks == 0) return hipSuccess;
+  local_wt_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(a, wt, n_ktiles, n_ntiles);
+  return hipGetLastError();
+}
+
 __global__ __launch_bounds__(256) void fill_zero_kernel(u32x4* p, int64_t n16) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x)
     p[i] = u32x4{0u, 0u, 0u, 0u};

@@ -59,11 +59,13 @@ __global__ __launch_bounds__(WB_WAVES * 64) void wb_gemm_kernel(WbArgs a, int m_
   __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * WB_STAGE];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // XCD-aware, grouped tile walk
-  const int total = m_tiles * n_tiles;
+  // XCD-aware, grouped tile walk (batches one after another)
+  const int per_batch = m_tiles * n_tiles;
+  const int total = per_batch * a.batch;
   const int per = (total + 7) / 8;
-  const int t = (int)(blockIdx.x % 8) * per + (int)(blockIdx.x / 8);
-  if (t >= total) return;
+  const int tb = (int)(blockIdx.x % 8) * per + (int)(blockIdx.x / 8);
+  if (tb >= total) return;
+  const int bt = tb / per_batch, t = tb % per_batch;
   const int group = t / (WB_GM * n_tiles), rem = t % (WB_GM * n_tiles);
   const int gm = std::min(WB_GM, m_tiles - group * WB_GM);
   const int mt = group * WB_GM + rem % gm, nt = rem / gm;
@@ -74,9 +76,11 @@ __global__ __launch_bounds__(WB_WAVES * 64) void wb_gemm_kernel(WbArgs a, int m_
   // of a slice (L loads per wave), i.e. rows 8 (L w + j) + lane/8 of the tile at
   // slot lane%8, whose source is chunk (lane%8) ^ swz(row).  The load takes a
   // wave-uniform base (the wave's first row) plus a 32-bit lane offset; a wave's
-  // rows span 64 rows, so the offsets stay below 2^32 for d_in <= 16384.  Rows
-  // past the end are clamped to the last row (their results are not stored).
+  // rows span 64 rows, so the offsets stay below 2^32 for row strides up to
+  // 2^25 elements (the host checks).  Rows past the end are clamped to the last
+  // row (their results are not stored).
   const int K = a.d_in;
+  const int64_t ldz = a.ldz, ldw = a.ldw;
   const int wr0 = WB_LOADS * WB_RPL * (wave % WB_DMA_WAVES);
   const int64_t a_base_row = std::min<int64_t>(m0 + wr0, a.n_rows - 1);
   const int64_t b_base_row = std::min<int64_t>((int64_t)n0 + wr0, (int64_t)a.d_out - 1);
@@ -87,11 +91,11 @@ __global__ __launch_bounds__(WB_WAVES * 64) void wb_gemm_kernel(WbArgs a, int m_
     const int c = (lane & 7) ^ swz(r);
     const int64_t m = std::min<int64_t>(m0 + r, a.n_rows - 1);
     const int64_t n = std::min<int64_t>((int64_t)n0 + r, (int64_t)a.d_out - 1);
-    a_lo[j] = (uint32_t)((m - a_base_row) * K * 2 + c * 16);
-    b_lo[j] = (uint32_t)((n - b_base_row) * K * 2 + c * 16);
+    a_lo[j] = (uint32_t)((m - a_base_row) * ldz * 2 + c * 16);
+    b_lo[j] = (uint32_t)((n - b_base_row) * ldw * 2 + c * 16);
   }
-  const unsigned char* Abase = (const unsigned char*)a.z + a_base_row * (int64_t)K * 2;
-  const unsigned char* Bbase = (const unsigned char*)a.w_b + b_base_row * (int64_t)K * 2;
+  const unsigned char* Abase = (const unsigned char*)(a.z + bt * a.z_batch) + a_base_row * ldz * 2;
+  const unsigned char* Bbase = (const unsigned char*)(a.w_b + bt * a.w_batch) + b_base_row * ldw * 2;
 
   auto load_slice = [&](int kt) {
     if (wave >= WB_DMA_WAVES) return;
@@ -161,6 +165,7 @@ __global__ __launch_bounds__(WB_WAVES * 64) void wb_gemm_kernel(WbArgs a, int m_
   }
 
   // epilogue: lane holds column l32 of each 32x32 block, rows hk*4 + 8(e/4) + e%4
+  const int64_t ybase = bt * a.y_batch;
 #pragma unroll
   for (int i = 0; i < MI; ++i)
 #pragma unroll
@@ -172,9 +177,9 @@ __global__ __launch_bounds__(WB_WAVES * 64) void wb_gemm_kernel(WbArgs a, int m_
         const int64_t m = m0 + wm * 128 + i * 32 + hk * 4 + (e >> 2) * 8 + (e & 3);
         if (m >= a.n_rows) continue;
         if (OUT_BF16)
-          ((__bf16*)a.y)[m * a.d_out + n] = (__bf16)acc[i][j][e];
+          ((__bf16*)a.y)[ybase + m * a.ldy + n] = (__bf16)acc[i][j][e];
         else
-          ((float*)a.y)[m * a.d_out + n] = acc[i][j][e];
+          ((float*)a.y)[ybase + m * a.ldy + n] = acc[i][j][e];
       }
     }
 }
@@ -185,7 +190,7 @@ hipError_t launch_wb(const WbArgs& a, hipStream_t s) {
   if (a.n_rows == 0) return hipSuccess;
   const int m_tiles = (int)((a.n_rows + WB_BM - 1) / WB_BM);
   const int n_tiles = (a.d_out + WB_BN - 1) / WB_BN;
-  const int total = m_tiles * n_tiles;
+  const int total = m_tiles * n_tiles * a.batch;
   const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
   if (a.y_bf16)
     wb_gemm_kernel<true><<<grid, dim3(WB_WAVES * 64), 0, s>>>(a, m_tiles, n_tiles);
