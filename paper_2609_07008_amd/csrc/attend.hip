@@ -16,8 +16,12 @@
 //                   with transposing LDS loads, P^T is the S^T accumulator
 //                   rounded to bf16 in place (its lane layout is already the
 //                   MFMA operand layout once the keys are taken in the order
-//                   the V reads use)
-// and emits one normalized partial and one log-sum-exp per (slot, chunk).
+//                   the V reads use); with a rotary value (the whole latent row
+//                   is the value) also the d_r RoPE dims, whose sums live in the
+//                   workspace and are rotated back per segment (RestorePhase,
+//                   R^-1: Alg. 2, eq:offonline)
+// and emits one normalized partial and one log-sum-exp per (slot, chunk), or,
+// with one chunk per slot, the merged head output itself.
 // Tiles are fetched with 16-byte direct-to-LDS loads, double-buffered; the
 // 16-byte chunks of a key row are XOR-swizzled so row and column reads hit
 // distinct banks.
