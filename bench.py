@@ -333,29 +333,39 @@ def moe_fanout_bench(torch, stream, n_rows: int, n_experts: int = 256, tau: floa
 def shared_wb_bench(torch, stream, z, reps: int = 5):
     """mla_shared_wb: y = W_b z over every row of the workload, z the step's own
     bf16 output (mla_sliced_oproj_add_planned with a bf16 z), W_b [4096, 4096]
-    bf16 with std 0.02 drawn on the device, y fp32: median time and the MFMA
+    bf16 with std 0.02 drawn on the device, y fp32 (and, as a second figure, y
+    bf16, the output type of a bf16 serving stack): median time and the MFMA
     rate against the dense bf16 peak."""
     from paper_2609_07008_amd import mla
     n_rows, d = int(z.shape[0]), int(z.shape[1])
     g = torch.Generator(device="cuda")
     g.manual_seed(70082)
     w = (torch.randn((d, d), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
-    y = torch.empty((n_rows, d), dtype=torch.float32, device="cuda")
-    mla.shared_wb(z, w, y, stream=stream)
-    torch.cuda.synchronize()
-    ts = []
-    for _ in range(reps):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        mla.shared_wb(z, w, y, stream=stream)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ts.append(e0.elapsed_time(e1))
-    ms = float(np.median(ts))
     flop = 2.0 * n_rows * d * d
+
+    def timed(y):
+        mla.shared_wb(z, w, y, stream=stream)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            mla.shared_wb(z, w, y, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    y = torch.empty((n_rows, d), dtype=torch.float32, device="cuda")
+    ms = timed(y)
+    del y
+    y = torch.empty((n_rows, d), dtype=torch.bfloat16, device="cuda")
+    ms_bf16 = timed(y)
     del w, y
     return {"rows": n_rows, "d_in": d, "d_out": d, "ms": round(ms, 3), "flop": flop, "z": "the step's bf16 z",
-            "TFLOP_per_s": round(flop / (ms * 1e-3) / 1e12, 1), "frac_of_bf16_peak": round(flop / (ms * 1e-3) / 2.5e15, 4)}
+            "TFLOP_per_s": round(flop / (ms * 1e-3) / 1e12, 1), "frac_of_bf16_peak": round(flop / (ms * 1e-3) / 2.5e15, 4),
+            "y_bf16": {"ms": round(ms_bf16, 3), "TFLOP_per_s": round(flop / (ms_bf16 * 1e-3) / 1e12, 1),
+                       "frac_of_bf16_peak": round(flop / (ms_bf16 * 1e-3) / 2.5e15, 4)}}
 
 
 def dense_oproj(wl, out_o, dev, torch, stream, reps: int = 5):

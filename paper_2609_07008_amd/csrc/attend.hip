@@ -232,14 +232,16 @@ __device__ __forceinline__ void issue_tile(const void* kv, const SegInfo& s, int
 // this lane's query by R(t - p_s) into qf's RoPE steps; the angle is reduced in
 // double precision (in revolutions) and fed to the hardware sin/cos.  Returns
 // the lane's largest visible canonical offset in s (INT_MAX without a head-row).
-template <class C, int DC, int DR>
+template <class C, int DC, int DR, bool RELOAD = true>
 __device__ __forceinline__ int relocate_query(bf16x8 (&qf)[C::KS], const ItemView& v, const SegInfo& s, int half) {
   const int64_t delta = v.t_pos - s.req_offset;
   const int64_t lm = delta < s.length - 1 ? delta : s.length - 1;
   bf16x8 raw[C::RS];
 #pragma unroll
   for (int rs = 0; rs < C::RS; ++rs) {
-    if (DR == 16) {
+    if (!RELOAD) {
+      raw[rs] = qf[C::CS + rs];   // still the unrotated query
+    } else if (DR == 16) {
       const u32x2 lo = *(const u32x2*)(v.qsrc + DC + half * 4);
       const u32x2 hi = *(const u32x2*)(v.qsrc + DC + 8 + half * 4);
       raw[rs] = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
@@ -521,6 +523,13 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
   bool restarted = false;
   int attempt = 0;                  // passes made over the item (workgroup-uniform)
   if (tid == 0) restart_at = ~0u;   // ordered before any access by the first tile barrier
+  // the first attempt's relocation for the chunk's first segment, from the
+  // unrotated RoPE part still in qf
+  {
+    const SegInfo s0 = segs[rank_seg[chk.first_rank]];
+    lim = relocate_query<C, DC, DR, false>(qf, v, s0, half);
+    wave_lim = wave_min_i(lim);
+  }
   for (;;) {
 #pragma unroll
     for (int d = 0; d < C::OB; ++d)
@@ -537,8 +546,10 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
     n_keys = seg_keys(v, cs, rank_seg[c_rank] == it.seg);
     n_ntiles = (n_keys + C::BK - 1) / C::BK;
     n_tile = 0;
-    relocate(cs);
-    if (restarted) issue(L, cs, n_keys, 0);   // the first attempt's went out before the queries
+    if (restarted) {
+      relocate(cs);
+      issue(L, cs, n_keys, 0);   // the first attempt's went out before the queries
+    }
 
     if (ROT && active) rot_clear(rot());
     bool restart = false;
@@ -780,10 +791,20 @@ __global__ __launch_bounds__(256, 1) void attend_kernel(AttendArgs a) {
       const int nrow = it.count - wave * 32 < 32 ? it.count - wave * 32 : 32;   // valid rows of the wave
       const int64_t slot0 = (it.kind == 0 ? 0 : a.local_slot_base) + it.hr_begin + wave * 32;
       uint16_t* ob0 = (uint16_t*)a.out_direct + slot0 * a.dv;
-      for (int r0 = 0; r0 < nrow; r0 += 64 / LPR) {
-        const int r = r0 + lane / LPR, cl = lane % LPR;
-        if (r < nrow)
-          *(u32x4*)(ob0 + (int64_t)r * a.dv + cl * 8) = *(const u32x4 MLA_LDS*)(srow + r * SROW + cl * 8);
+      // rows of the wave in passes of 64 / LPR rows, eight passes' reads issued before
+      // their stores (rows past nrow read stale staging bytes and store nothing)
+      constexpr int RPI = 64 / LPR, NP = 32 / RPI, UB = NP < 8 ? NP : 8;
+      const int rl = lane / LPR, cl = lane % LPR;
+#pragma unroll
+      for (int p0 = 0; p0 < NP; p0 += UB) {
+        u32x4 t[UB];
+#pragma unroll
+        for (int j = 0; j < UB; ++j) t[j] = *(const u32x4 MLA_LDS*)(srow + ((p0 + j) * RPI + rl) * SROW + cl * 8);
+#pragma unroll
+        for (int j = 0; j < UB; ++j) {
+          const int r = (p0 + j) * RPI + rl;
+          if (r < nrow) *(u32x4*)(ob0 + (int64_t)r * a.dv + cl * 8) = t[j];
+        }
       }
       if (!valid) return;
       uint16_t* ob = (uint16_t*)a.out_direct + slot * a.dv;
