@@ -408,6 +408,46 @@ def dense_oproj(wl, out_o, dev, torch, stream, reps: int = 5):
             "w_o": f"dense [1, {g.n_heads * g.d_latent}, {g.d_model}] bf16"}
 
 
+def device_peaks(torch, stream, att_tflops: float, oproj_gbs: float, reps: int = 3):
+    """The rates measured on this device that the step's kernels are set against,
+    beside the data-sheet figures: the dense bf16 matrix-core rate from
+    mla_probe_mfma_bf16 (waves doing nothing but MFMA 32x32x16 bf16), and a device
+    copy's HBM rate (torch's copy of 2 GiB of float32: half reads, half writes)."""
+    from paper_2609_07008_amd import mla
+    sink = torch.zeros(4, dtype=torch.float32, device="cuda")
+    mla.probe_mfma_bf16(200, sink, stream=stream)
+    torch.cuda.synchronize()
+    ts = []
+    flop = 0.0
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        flop = mla.probe_mfma_bf16(4000, sink, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) / 1e3)
+    mfma = flop / float(np.median(ts)) / 1e12
+    n = 1 << 29
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps + 2):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        y.copy_(x)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) / 1e3)
+    copy = 2 * n * 4 / float(np.median(ts)) / 1e12
+    del x, y, sink
+    return {"mfma_bf16_TFLOP_per_s": round(mfma, 1), "mfma_probe": "mla_probe_mfma_bf16, 4000 products per chain",
+            "attention_frac_of_measured_mfma": round(att_tflops / mfma, 4),
+            "copy_TB_per_s": round(copy, 3), "copy": "torch copy_ of 2 GiB float32",
+            "oproj_add_frac_of_copy": round(oproj_gbs / 1e3 / copy, 4)}
+
+
 def host_plan_step(wl, dev, torch, stream, split: int, reps: int = 3):
     """The same step through the host-plan entry points (mla_online_attend, which
     builds and uploads its plan from the host on every call, writes f32 partials,
@@ -692,6 +732,7 @@ def main():
         out["offline_producer"] = offline_producer(wl, torch, stream)
     out["protected_set"] = protected_set(wl, torch, stream)
     out["moe_fanout"] = moe_fanout_bench(torch, stream, wl.n_rows)
+    out["device_peaks"] = device_peaks(torch, stream, att_tflops, out["hbm_gbs"]["oproj_add"])
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmla_online.so")
-SOURCES = ["api.hip", "attend.hip", "dplan.hip", "merge.hip", "moe.hip", "oproj.hip", "protect.hip", "wb.hip"]
+SOURCES = ["api.hip", "attend.hip", "dplan.hip", "merge.hip", "moe.hip", "oproj.hip", "probe.hip", "protect.hip", "wb.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -13,8 +13,10 @@
 #include <vector>
 
 #include "common.h"
+#include "mla_probe.h"
 #include "moe.h"
 #include "oproj.h"
+#include "probe.h"
 #include "protect.h"
 #include "wb.h"
 
@@ -1394,6 +1396,25 @@ mla_status mla_shared_wb(int64_t n_rows, int32_t d_in, int32_t d_out, const void
   a.ldy = d_out;
   const hipError_t e = mla::launch_wb(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "shared W_b kernel");
+  return MLA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// diagnostic: the on-device bf16 matrix-core rate
+// ---------------------------------------------------------------------------
+mla_status mla_probe_mfma_bf16(int32_t iters, double* flop, float* sink, void* stream) {
+  g_detail.clear();
+  if (flop == nullptr || sink == nullptr) return fail(MLA_ERR_NULL, "flop and sink are required");
+  if (iters < 1 || iters > (1 << 24)) return fail(MLA_ERR_SHAPE, "iters = %d outside [1, 2^24]", iters);
+  int dev = 0, n_cu = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if ((e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+    return hip_fail(e, "hipDeviceGetAttribute");
+  const int n_wg = 2 * n_cu;   // two workgroups of 4 waves per compute unit: two waves per SIMD
+  *flop = (double)n_wg * mla::kProbeWaves * mla::kProbeChains * (double)iters * 32768.0;
+  if ((e = mla::launch_probe_mfma(iters, n_wg, sink, reinterpret_cast<hipStream_t>(stream))) != hipSuccess)
+    return hip_fail(e, "probe kernel");
   return MLA_OK;
 }
 

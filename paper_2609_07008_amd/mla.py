@@ -24,7 +24,8 @@ EXPORTS = ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", 
            "mla_online_attend_planned_noalloc", "mla_sliced_oproj_add_planned",
            "mla_offline_produce_query", "mla_offline_produce", "mla_protected_rows_query", "mla_protected_rows",
            "mla_protected_rows_planned_query", "mla_protected_rows_planned",
-           "mla_moe_fanout", "mla_shared_wb", "mla_status_str", "mla_last_error_detail", "mla_version")
+           "mla_moe_fanout", "mla_shared_wb", "mla_probe_mfma_bf16", "mla_status_str", "mla_last_error_detail",
+           "mla_version")
 
 
 class MlaError(RuntimeError):
@@ -83,11 +84,13 @@ def _load(path: str = LIB_PATH):
     lib.mla_protected_rows_planned.argtypes = [IP, P, ctypes.POINTER(ProtectCfg), P, P, P, P, P, SZ, P]
     lib.mla_moe_fanout.argtypes = [I64, I32, P, I32, I32, ctypes.c_float, P, P, P, P, P]
     lib.mla_shared_wb.argtypes = [I64, I32, I32, P, P, I32, P, P]
+    lib.mla_probe_mfma_bf16.argtypes = [I32, ctypes.POINTER(ctypes.c_double), P, P]
     for f in ("mla_online_attend_query", "mla_online_attend", "mla_segment_merge", "mla_sliced_oproj_add",
               "mla_online_plan_query", "mla_online_plan", "mla_online_attend_planned",
               "mla_online_attend_planned_noalloc", "mla_sliced_oproj_add_planned", "mla_offline_produce_query",
               "mla_offline_produce", "mla_protected_rows_query", "mla_protected_rows",
-              "mla_protected_rows_planned_query", "mla_protected_rows_planned", "mla_moe_fanout", "mla_shared_wb"):
+              "mla_protected_rows_planned_query", "mla_protected_rows_planned", "mla_moe_fanout", "mla_shared_wb",
+              "mla_probe_mfma_bf16"):
         getattr(lib, f).restype = ctypes.c_int
     lib.mla_status_str.argtypes = [ctypes.c_int]
     lib.mla_status_str.restype = ctypes.c_char_p
@@ -312,6 +315,15 @@ def shared_wb(z, w_b, y, stream=None):
     d_out = int(w_b.shape[0])
     out = MLA_BF16 if y.dtype == torch.bfloat16 else MLA_F32
     _check(LIB.mla_shared_wb(n, d_in, d_out, _ptr(z), _ptr(w_b), out, _ptr(y), _stream(stream)))
+
+
+def probe_mfma_bf16(iters, sink, stream=None) -> float:
+    """Enqueue the matrix-core rate probe (mla_probe_mfma_bf16, a diagnostic of
+    mla_probe.h) with `iters` products per chain; sink is a device tensor of at
+    least 4 bytes.  Returns the launch's flop; time it with events on `stream`."""
+    flop = ctypes.c_double(0.0)
+    _check(LIB.mla_probe_mfma_bf16(int(iters), ctypes.byref(flop), _ptr(sink), _stream(stream)))
+    return flop.value
 
 
 def version() -> str:

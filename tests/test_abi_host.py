@@ -12,7 +12,7 @@ from oracle import mla_oracle as M
 from workloads import make_custom, make_workload
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "mla_online.h")
+HEADERS = sorted(os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h"))
 
 
 @pytest.fixture(scope="module")
@@ -22,15 +22,18 @@ def mla():
 
 
 def header_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(mla_[a-z_]+)\s*\(", text)))
+    """every function declared by the headers under include/"""
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names.update(re.findall(r"\b(mla_[a-z0-9_]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_exports_every_declared_symbol(mla):
     declared = header_functions()
     assert "mla_online_attend" in declared and "mla_segment_merge" in declared
-    assert "mla_sliced_oproj_add" in declared
+    assert "mla_sliced_oproj_add" in declared and "mla_probe_mfma_bf16" in declared
     for name in declared:
         assert hasattr(mla.LIB, name), name
     assert set(declared) == set(mla.EXPORTS)
@@ -402,3 +405,13 @@ def test_noalloc_refuses_a_plan_larger_than_its_scratch(mla):
     st = mla.LIB.mla_online_attend_planned_noalloc(ctypes.byref(g), ctypes.byref(info), fake, fake, fake, fake, fake,
                                                    fake, 0, fake, None, None, None, None, None, None)
     assert st == 6 and "scratch" in mla.LIB.mla_last_error_detail().decode()
+
+
+def test_probe_validates_before_any_device_work(mla):
+    flop = ctypes.c_double(0.0)
+    sink = ctypes.c_void_p(256)   # never dereferenced: every call below fails validation first
+    assert mla.LIB.mla_probe_mfma_bf16(0, ctypes.byref(flop), sink, None) == 2
+    assert mla.LIB.mla_probe_mfma_bf16((1 << 24) + 1, ctypes.byref(flop), sink, None) == 2
+    assert mla.LIB.mla_probe_mfma_bf16(10, None, sink, None) == 1
+    assert mla.LIB.mla_probe_mfma_bf16(10, ctypes.byref(flop), None, None) == 1
+    assert flop.value == 0.0

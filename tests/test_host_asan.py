@@ -10,7 +10,7 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2609_07008_amd", "csrc")
-SOURCES = ["api.hip", "attend.hip", "dplan.hip", "merge.hip", "moe.hip", "oproj.hip", "protect.hip", "wb.hip"]
+from paper_2609_07008_amd.build import SOURCES   # every source of the library
 
 
 def _hipcc():
