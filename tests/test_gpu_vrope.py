@@ -66,7 +66,7 @@ def test_vrope_one_row(tq, prot):
     check("z_off (f32)", produce(wl, "f32"), M.artifact(wl))
 
 
-@pytest.mark.parametrize("cfg,split", [(2, 0), (2, 10 ** 9), (5, 10 ** 9)])
+@pytest.mark.parametrize("cfg,split", [(2, 0), (2, 10 ** 9), (3, 8192), (3, 10 ** 9), (4, 10 ** 9), (5, 10 ** 9)])
 def test_vrope_full_workload(cfg, split):
     wl = make_workload(cfg, value_rope=True)
     split = min(split, wl.n_rows) if split else 0
