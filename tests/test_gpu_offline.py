@@ -67,15 +67,19 @@ def test_offline_artifact_feeds_the_online_step():
     compare_rows(wl, st, np.arange(wl.n_rows), z_ref)
 
 
-def test_offline_full_size_sampled():
-    """The producer at the benchmark's 256K geometry and launch (64 x 4096-token
-    documents + 2048 query rows, 56 Local heads, bf16 artifact), inputs drawn on
-    the device as the benchmark draws them; sampled rows (segment starts and
-    ends, tile edges, query rows, random rows) against the oracle's canonical
-    artifact computed from the same values copied back."""
+@pytest.mark.parametrize("cfg", [4, 5])
+def test_offline_full_size_sampled(cfg):
+    """The producer at full size: the benchmark's 256K geometry and launch (64 x
+    4096-token documents + 2048 query rows, 56 Local heads, 512 channels per
+    projection group) and the 128-head workload (32 x 2048-token documents, 112
+    Local heads, 16 projection groups of 448 channels: a ragged last column
+    tile), bf16 artifact, inputs drawn on the device as the benchmark draws them;
+    sampled rows (segment starts and ends, tile edges, query rows, random rows)
+    against the oracle's canonical artifact computed from the same values copied
+    back."""
     import torch
     from paper_2609_07008_amd import mla
-    wl = make_workload(5)
+    wl = make_workload(cfg)
     g = wl.geom
     n, hl = wl.n_rows, g.heads_per_group - 1
     gen = torch.Generator(device="cuda")
@@ -101,8 +105,9 @@ def test_offline_full_size_sampled():
     segs = np.asarray(wl.segs)
     rng = np.random.default_rng(11)
     picks = []                                   # (segment, canonical u)
-    for s in [0, 1, 31, 63]:
-        picks += [(s, u) for u in (0, 1, 63, 64, 65, 127, 2047, 4095)]
+    n_docs = len(segs) - 1
+    for s in [0, 1, n_docs // 2, n_docs - 1]:
+        picks += [(s, u) for u in (0, 1, 63, 64, 65, 127, 2047, 4095) if u < segs[s, 1]]
     q_seg = int(np.argmax(segs[:, 2]))           # the query block (last in request order)
     picks += [(q_seg, u) for u in (0, 1, 1000, int(segs[q_seg, 1]) - 1)]
     picks += [(int(s), int(rng.integers(0, segs[s, 1]))) for s in rng.integers(0, len(segs), size=8)]
