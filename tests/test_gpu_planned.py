@@ -165,7 +165,8 @@ def test_planned_tiny_and_f32_output():
 
 
 @pytest.mark.parametrize("cfg,split,cap", [(2, 0, "exact"), (2, 10 ** 9, "all_rows"), (3, 8192, "exact"),
-                                           (5, 10 ** 9, "exact_plus")])
+                                           (4, 10 ** 9, "all_rows"), (5, 10 ** 9, "exact_plus"),
+                                           (5, 10 ** 9, "all_rows")])
 def test_planned_full_workload(cfg, split, cap):
     from paper_2609_07008_amd import device_inputs
     wl = make_workload(cfg)
