@@ -234,6 +234,40 @@ def test_chained_protected_set_step_and_wb():
     check("y = W_b z", y_gpu, M.shared_wb(ref.z, w64))
 
 
+def test_step_bf16_z_and_wb_full_size():
+    """The benchmark's hand-off at full size: the 256K step on the plan-once path
+    (capacity = every row) writing z in bf16, then y = W_b z (4096 -> 4096) over
+    every row; on sampled rows (segment edges, protected rows) z against the
+    oracle, y against W_b applied to the step's own z (the kernel's bound) and to
+    the oracle's z."""
+    import torch
+    from paper_2609_07008_amd import device_inputs, mla, step
+    wl = make_workload(5)
+    g = wl.geom
+    n = wl.n_rows
+    inputs = device_inputs.upload(wl)
+    st = step.PlannedStep(g, wl.segs, wl.glob_head, n, n, z_dtype=torch.bfloat16)
+    prot_d, n_d = _device_prot(wl, n)
+    st.run(prot_d, n_d, inputs["kv"], inputs["q_glob"], _q_loc_padded(inputs, wl, n), inputs["w_o"],
+           inputs["z_off"])
+    w_b_in = wb_inputs(1, g.d_model, g.d_model, seed=64)[1]
+    w_b = device_inputs.to_bf16(w_b_in)
+    y = torch.empty((n, g.d_model), dtype=torch.float32, device="cuda")
+    mla.shared_wb(st.z, w_b, y)
+    torch.cuda.synchronize()
+    assert int(st.status.item()) == 0
+    kv = wl.kv()
+    keys = M.TrueKeys(kv, wl.segs, g.d_latent, g.rope_base)
+    rows = np.asarray(segment_edge_sample(wl, seed=64), dtype=np.int64)
+    ref = compare_rows(wl, st, rows, None, kv=kv, keys=keys)
+    z_gpu = st.z[rows].float().cpu().numpy().astype(np.float64)
+    y_gpu = y[rows].cpu().numpy().astype(np.float64)
+    w64 = w_b_in.astype(np.float64)
+    bound = 3e-4 * (np.abs(z_gpu) @ np.abs(w64).T) + 1e-7
+    assert np.all(np.abs(y_gpu - M.shared_wb(z_gpu, w64)) <= bound)
+    check("y = W_b z (256K, sampled)", y_gpu, M.shared_wb(ref.z, w64))
+
+
 @pytest.mark.parametrize("case", ["over_capacity", "negative_count", "unsorted", "duplicate", "row_past_end",
                                   "negative_row"])
 def test_device_list_rejected(case):
